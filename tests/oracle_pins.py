@@ -1,0 +1,303 @@
+"""Pins of the CPU oracle against facts the mathematics fixes (not against itself).
+
+Each ``pin_*`` function takes a loaded ``oracle.Oracle`` and raises
+AssertionError when the oracle disagrees with:
+
+* exact big-integer / rational brute force on tiny inputs,
+* closed forms (all-ones, extreme int8 values, an index-structured sum),
+* textbook identities (identity and permutation matrices),
+* the transpose invariant C^T = B^T A^T (bit-identical),
+* split-K linearity, thread-count invariance, the int32 range check,
+* numpy's int64 matmul as an independent library GEMM.
+
+The same functions run against deliberately broken oracle builds in
+``test_oracle_mutants.py``: each plausible mistake must trip at least one pin.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+from paper_2512_13282_amd import inputs
+
+RNG = np.random.default_rng
+
+
+def _strided(x: np.ndarray, pad: int) -> np.ndarray:
+    """Same values, row stride cols + pad (a view into a wider buffer)."""
+    buf = np.zeros((x.shape[0], x.shape[1] + pad), dtype=x.dtype)
+    buf[:, : x.shape[1]] = x
+    return buf[:, : x.shape[1]]
+
+
+# ----------------------------------------------------------------------------- int8
+def pin_i8_bruteforce_tiny(o):
+    """All (M, N, K) in {0..4}^3 against Python big-int sums, mixed strides/threads."""
+    rng = RNG(11)
+    for M in range(5):
+        for N in range(5):
+            for K in range(5):
+                A = rng.integers(-128, 128, size=(M, K), dtype=np.int8)
+                B = rng.integers(-128, 128, size=(K, N), dtype=np.int8)
+                pad = (M + N + K) % 3
+                Av, Bv = _strided(A, pad), _strided(B, 2 - pad % 2)
+                C, ovf = o.gemm_i8_i32(Av, Bv, nthreads=1 + (M % 3), ldc_pad=pad)
+                assert ovf == 0
+                for i in range(M):
+                    for j in range(N):
+                        exact = sum(int(A[i, k]) * int(B[k, j]) for k in range(K))
+                        assert int(C[i, j]) == exact, (M, N, K, i, j)
+
+
+def pin_i8_extremes_bruteforce(o):
+    """Operands drawn only from {-128, -1, 0, 1, 127} on a ragged shape."""
+    rng = RNG(12)
+    vals = np.array([-128, -1, 0, 1, 127], dtype=np.int8)
+    M, N, K = 7, 9, 13
+    A = vals[rng.integers(0, 5, size=(M, K))]
+    B = vals[rng.integers(0, 5, size=(K, N))]
+    C, _ = o.gemm_i8_i32(A, B, nthreads=3)
+    for i in range(M):
+        for j in range(N):
+            assert int(C[i, j]) == sum(int(A[i, k]) * int(B[k, j]) for k in range(K))
+
+
+def pin_i8_closed_forms(o):
+    """ones.ones = K; (-128)(-128)K = 16384K; (-128)(127)K = -16256K."""
+    for K in (1, 5, 64, 1000):
+        C, _ = o.gemm_i8_i32(np.ones((3, K), np.int8), np.ones((K, 4), np.int8))
+        assert (C == K).all()
+        C, _ = o.gemm_i8_i32(np.full((2, K), -128, np.int8), np.full((K, 3), -128, np.int8))
+        assert (C == 16384 * K).all()
+        C, _ = o.gemm_i8_i32(np.full((2, K), -128, np.int8), np.full((K, 3), 127, np.int8))
+        assert (C == -16256 * K).all()
+    # the largest K of the workload sweep: 16384 * 14336 = 234,881,024 still fits int32
+    C, ovf = o.gemm_i8_i32(np.full((1, 14336), -128, np.int8), np.full((14336, 2), -128, np.int8))
+    assert ovf == 0 and (C == 234881024).all()
+
+
+def pin_i8_index_structured(o):
+    """A[i][k] = i - k, B[k][j] = k + 3j (asymmetric in every index), closed form:
+    sum_k (i-k)(k+3j) = i*S1 + 3ijK - S2 - 3j*S1, S1 = K(K-1)/2, S2 = (K-1)K(2K-1)/6."""
+    M, N, K = 23, 29, 37
+    i = np.arange(M)[:, None]
+    k = np.arange(K)
+    A = (i - k[None, :]).astype(np.int8)
+    j = np.arange(N)[None, :]
+    B = (k[:, None] + 3 * j).astype(np.int8)
+    assert A.min() >= -128 and B.max() <= 127
+    C, _ = o.gemm_i8_i32(_strided(A, 5), B, nthreads=4, ldc_pad=3)
+    S1, S2 = K * (K - 1) // 2, (K - 1) * K * (2 * K - 1) // 6
+    expect = i * S1 + 3 * i * j * K - S2 - 3 * j * S1
+    assert (C == expect).all()
+
+
+def pin_i8_identity_permutation(o):
+    """A.I = A, I.B = B, P.B permutes rows of B, A.Q permutes columns of A."""
+    rng = RNG(13)
+    M, K, N = 17, 19, 11
+    A = rng.integers(-128, 128, size=(M, K), dtype=np.int8)
+    B = rng.integers(-128, 128, size=(K, N), dtype=np.int8)
+    C, _ = o.gemm_i8_i32(A, np.eye(K, dtype=np.int8))
+    assert (C == A).all()
+    C, _ = o.gemm_i8_i32(np.eye(K, dtype=np.int8), B)
+    assert (C == B).all()
+    perm = rng.permutation(K)
+    P = np.zeros((K, K), np.int8)
+    P[np.arange(K), perm] = 1            # (P.B)[r] = B[perm[r]]
+    C, _ = o.gemm_i8_i32(P, B)
+    assert (C == B[perm]).all()
+    Q = np.zeros((K, K), np.int8)
+    Q[perm, np.arange(K)] = 1            # (A.Q)[:, c] = A[:, perm[c]]
+    C, _ = o.gemm_i8_i32(A, Q)
+    assert (C == A[:, perm]).all()
+
+
+def pin_i8_transpose_invariant(o):
+    """C^T == oracle(B^T, A^T), element for element."""
+    M, N, K = 31, 45, 53
+    A, B = inputs.make_inputs("int8", M, N, K, seed=21)
+    C, _ = o.gemm_i8_i32(A, B, nthreads=3)
+    Ct, _ = o.gemm_i8_i32(np.ascontiguousarray(B.T), np.ascontiguousarray(A.T), nthreads=5)
+    assert (C.T == Ct).all()
+
+
+def pin_i8_numpy_library(o):
+    """Against numpy's int64 matmul on a multi-row, strided, ragged problem."""
+    M, N, K = 67, 131, 259
+    A, B = inputs.make_inputs("int8", M, N, K, seed=22)
+    C, ovf = o.gemm_i8_i32(_strided(A, 9), _strided(B, 3), nthreads=7, ldc_pad=5)
+    ref = A.astype(np.int64) @ B.astype(np.int64)
+    assert ovf == 0 and (C == ref).all()
+    C64 = o.gemm_i8_i64(A, B, nthreads=2, ldc_pad=1)
+    assert (C64 == ref).all()
+
+
+def pin_i8_split_k_linearity(o):
+    """oracle(A, B) == oracle(A[:, :s], B[:s]) + oracle(A[:, s:], B[s:])."""
+    M, N, K = 12, 14, 100
+    A, B = inputs.make_inputs("int8", M, N, K, seed=23)
+    C, _ = o.gemm_i8_i32(A, B)
+    s = 37
+    C1, _ = o.gemm_i8_i32(np.ascontiguousarray(A[:, :s]), np.ascontiguousarray(B[:s]))
+    C2, _ = o.gemm_i8_i32(np.ascontiguousarray(A[:, s:]), np.ascontiguousarray(B[s:]))
+    assert (C == C1.astype(np.int64) + C2).all()
+
+
+def pin_i8_thread_invariance(o):
+    M, N, K = 29, 33, 41
+    A, B = inputs.make_inputs("int8", M, N, K, seed=24)
+    ref, _ = o.gemm_i8_i32(A, B, nthreads=1)
+    for t in (2, 3, 8, 29, 64):
+        C, _ = o.gemm_i8_i32(A, B, nthreads=t)
+        assert (C == ref).all(), t
+
+
+def pin_i8_overflow_detection(o):
+    """K = 131072 of (-128)(-128) sums to 2^31 (one past INT32_MAX); K = 131071 fits;
+    140000 of (-128)(127) is below INT32_MIN."""
+    K = 131072
+    C, ovf = o.gemm_i8_i32(np.full((2, K), -128, np.int8), np.full((K, 3), -128, np.int8))
+    assert ovf == 6
+    assert (C == np.int32(-(2 ** 31))).all()          # 2^31 wrapped modulo 2^32
+    C, ovf = o.gemm_i8_i32(np.full((1, K - 1), -128, np.int8), np.full((K - 1, 1), -128, np.int8))
+    assert ovf == 0 and int(C[0, 0]) == 16384 * (K - 1) == 2147467264
+    K = 140000
+    C, ovf = o.gemm_i8_i32(np.full((1, K), -128, np.int8), np.full((K, 2), 127, np.int8))
+    assert ovf == 2
+    assert int(C[0, 0]) == ((-16256 * K + 2 ** 31) % 2 ** 32) - 2 ** 31
+    C64 = o.gemm_i8_i64(np.full((1, K), -128, np.int8), np.full((K, 2), 127, np.int8))
+    assert (C64 == -16256 * K).all()
+
+
+def pin_freivalds(o):
+    """Freivalds accepts the exact product and rejects any single wrong element."""
+    M, N, K = 40, 50, 60
+    A, B = inputs.make_inputs("int8", M, N, K, seed=25)
+    ref = (A.astype(np.int64) @ B.astype(np.int64)).astype(np.int32)
+    assert o.freivalds_i8_i32(A, B, ref, trials=3) == 0
+    for (i, j) in ((0, 0), (M - 1, N - 1), (17, 3)):
+        bad = ref.copy()
+        bad[i, j] += 1
+        assert o.freivalds_i8_i32(A, B, bad, trials=2) > 0, (i, j)
+    # a strided C view is read with its own stride
+    wide = np.zeros((M, N + 7), np.int32)
+    wide[:, :N] = ref
+    assert o.freivalds_i8_i32(A, B, wide[:, :N], trials=2) == 0
+
+
+# ----------------------------------------------------------------------------- bf16
+def _frac_bf16(bits: int) -> Fraction:
+    return Fraction(float(inputs.f32_from_bf16_bits(np.array([bits], np.uint16))[0]))
+
+
+def pin_bf16_widening(o):
+    """Known bf16 encodings: sign, exponent bias 127, 7 fraction bits."""
+    cases = {0x3F80: 1.0, 0xC000: -2.0, 0x3FC0: 1.5, 0x4049: 3.140625, 0x0000: 0.0,
+             0x7F7F: (2 - 2 ** -7) * 2.0 ** 127, 0x0080: 2.0 ** -126, 0x0001: 2.0 ** -133,
+             0x3B80: 2.0 ** -8, 0xBF81: -(1 + 2 ** -7)}
+    for bits, val in cases.items():
+        assert o.bf16_to_double(bits) == val, hex(bits)
+    assert math.copysign(1.0, o.bf16_to_double(0x8000)) == -1.0
+
+
+def pin_bf16_exact_rational_tiny(o):
+    """All (M, N, K) in {0..4}^3: |oracle - exact| <= (K-1) u sum|ab|, u = 2^-53
+    (recursive-summation bound; products are exact), exact sums by Fraction."""
+    rng = RNG(31)
+    for M in range(5):
+        for N in range(5):
+            for K in range(5):
+                A = inputs.bf16_bits_from_f32(rng.standard_normal((M, K), dtype=np.float32) * 3)
+                B = inputs.bf16_bits_from_f32(rng.standard_normal((K, N), dtype=np.float32) * 3)
+                C = o.gemm_bf16_f64(_strided(A, 1), B, nthreads=2, ldc_pad=K % 2)
+                for i in range(M):
+                    for j in range(N):
+                        terms = [_frac_bf16(int(A[i, k])) * _frac_bf16(int(B[k, j])) for k in range(K)]
+                        exact = sum(terms, Fraction(0))
+                        bound = max(K - 1, 0) * Fraction(1, 2 ** 53) * sum(abs(t) for t in terms)
+                        assert abs(Fraction(float(C[i, j])) - exact) <= bound, (M, N, K, i, j)
+
+
+def pin_bf16_exact_rational_wide_range(o):
+    """Products spanning ~2^60 of dynamic range, where an fp32 accumulator would lose
+    terms: fp64 must stay within its bound of the exact rational sum."""
+    rng = RNG(32)
+    M, N, K = 5, 6, 24
+    A32 = (rng.standard_normal((M, K)) * np.exp2(rng.integers(-30, 30, size=(M, K)))).astype(np.float32)
+    B32 = (rng.standard_normal((K, N)) * np.exp2(rng.integers(-30, 30, size=(K, N)))).astype(np.float32)
+    A, B = inputs.bf16_bits_from_f32(A32), inputs.bf16_bits_from_f32(B32)
+    C = o.gemm_bf16_f64(A, B)
+    for i in range(M):
+        for j in range(N):
+            terms = [_frac_bf16(int(A[i, k])) * _frac_bf16(int(B[k, j])) for k in range(K)]
+            exact = sum(terms, Fraction(0))
+            bound = (K - 1) * Fraction(1, 2 ** 53) * sum(abs(t) for t in terms)
+            assert abs(Fraction(float(C[i, j])) - exact) <= bound, (i, j)
+
+
+def pin_bf16_integer_exact(o):
+    """Integer-valued bf16 operands: every sum is an exact integer, equal to the int64 GEMM."""
+    M, N, K = 19, 23, 301
+    A = inputs.small_int_bf16_matrix(M, K, seed=33)
+    B = inputs.small_int_bf16_matrix(K, N, seed=34)
+    C = o.gemm_bf16_f64(A, B, nthreads=3)
+    Ai = inputs.f32_from_bf16_bits(A).astype(np.int64)
+    Bi = inputs.f32_from_bf16_bits(B).astype(np.int64)
+    assert (C == (Ai @ Bi).astype(np.float64)).all()
+
+
+def pin_bf16_closed_forms(o):
+    one = int(inputs.bf16_bits_from_f32(np.array([1.0], np.float32))[0])
+    mhalf = int(inputs.bf16_bits_from_f32(np.array([-0.5], np.float32))[0])
+    for K in (1, 7, 256, 4097):
+        C = o.gemm_bf16_f64(np.full((2, K), one, np.uint16), np.full((K, 3), one, np.uint16))
+        assert (C == K).all()
+        C = o.gemm_bf16_f64(np.full((2, K), mhalf, np.uint16), np.full((K, 3), one, np.uint16))
+        assert (C == -0.5 * K).all()
+
+
+def pin_bf16_identity_permutation(o):
+    M, K, N = 9, 12, 10
+    A, B = inputs.make_inputs("bf16", M, N, K, seed=35)
+    one = int(inputs.bf16_bits_from_f32(np.array([1.0], np.float32))[0])
+    eye = np.where(np.eye(K, dtype=bool), one, 0).astype(np.uint16)
+    C = o.gemm_bf16_f64(A, eye)
+    assert (C == inputs.f32_from_bf16_bits(A).astype(np.float64)).all()
+    C = o.gemm_bf16_f64(eye, B)
+    assert (C == inputs.f32_from_bf16_bits(B).astype(np.float64)).all()
+    perm = RNG(36).permutation(K)
+    P = np.zeros((K, K), np.uint16)
+    P[np.arange(K), perm] = one
+    C = o.gemm_bf16_f64(P, B)
+    assert (C == inputs.f32_from_bf16_bits(B[perm]).astype(np.float64)).all()
+
+
+def pin_bf16_transpose_invariant(o):
+    """Same products (multiplication commutes), same k order: bit-identical."""
+    M, N, K = 21, 34, 77
+    A, B = inputs.make_inputs("bf16", M, N, K, seed=37)
+    C = o.gemm_bf16_f64(A, B, nthreads=2)
+    Ct = o.gemm_bf16_f64(np.ascontiguousarray(B.T), np.ascontiguousarray(A.T), nthreads=3)
+    assert np.array_equal(C.T.view(np.uint64), Ct.view(np.uint64))
+
+
+def pin_bf16_sequential_order(o):
+    """The fp64 sum runs k ascending: reversing k changes some results, and the
+    oracle matches the ascending left-to-right sum bit for bit."""
+    M, N, K = 3, 4, 50
+    A, B = inputs.make_inputs("bf16", M, N, K, seed=38)
+    C = o.gemm_bf16_f64(A, B)
+    Af = inputs.f32_from_bf16_bits(A).astype(np.float64)
+    Bf = inputs.f32_from_bf16_bits(B).astype(np.float64)
+    for i in range(M):
+        for j in range(N):
+            s = 0.0
+            for k in range(K):
+                s += Af[i, k] * Bf[k, j]
+            assert C[i, j] == s
+
+
+PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
