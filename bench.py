@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Throughput of the MI355X GEMM library on the paper-shaped workload sweep.
+
+Default run (one GPU): the int8 -> int32 GEMM at M = N = K = 8192 (headline
+`value`, TOPS) and the bf16 -> fp32 GEMM at the same size (the `bf16` object),
+inputs resident in HBM, W untimed warm-up launches, then K timed launches
+bracketed by device synchronisation.  Prints ONE JSON line on stdout with a
+roofline object for the dominant kernel (HIP events on the launch stream) and
+the CPU oracle timed on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--size S] [--sweep]
+
+`--sweep` also times every workload of the sweep (one JSON row each, on
+stderr and in gpurun_out/sweep.jsonl); memory-bound shapes there rotate
+through enough copies of B to defeat the 256 MB last-level cache.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (AMD published)
+HBM_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2512_13282_amd", "csrc", "gemm_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--size", type=int, default=8192)
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--only", choices=["int8", "bf16"], default=None)
+    return ap.parse_args()
+
+
+def kernel_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+
+
+def traffic_for(dtype: str, M: int, N: int, K: int):
+    """HBM bytes per launch from committed rocprofv3 FETCH_SIZE/WRITE_SIZE counters, or None
+    when none were taken for this workload or the kernel source changed since."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_sha():
+        return None
+    rec = t.get("workloads", {}).get(f"{dtype}_{M}x{K}x{N}")
+    return None if rec is None else rec.get("bytes_per_launch")
+
+
+class Workload:
+    def __init__(self, dtype, M, N, K, copies=1, seed=0):
+        import torch
+        from paper_2512_13282_amd import binding, inputs
+        self.dtype, self.M, self.N, self.K = dtype, M, N, K
+        self.b = binding
+        A, B = inputs.make_inputs(dtype, M, N, K, seed=seed)
+        self.A_host, self.B_host = A, B
+        dev = torch.device("cuda:0")
+        to = (lambda x: torch.from_numpy(x).to(dev)) if dtype == "int8" else \
+             (lambda x: torch.from_numpy(x.view(np.int16)).to(dev))
+        self.dA = to(A)
+        self.dBs = [to(B)] + [to(B).clone() for _ in range(copies - 1)]
+        self.dC = torch.empty((M, N), dtype=torch.int32 if dtype == "int8" else torch.float32, device=dev)
+        self.fn = binding.gemm_i8_i32 if dtype == "int8" else binding.gemm_bf16_f32
+        self.stream = torch.cuda.current_stream(dev)
+        self.i = 0
+
+    def launch(self):
+        dB = self.dBs[self.i % len(self.dBs)]
+        self.i += 1
+        rc = self.fn(self.M, self.N, self.K, self.dA.data_ptr(), self.K, dB.data_ptr(), self.N,
+                     self.dC.data_ptr(), self.N, self.stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(self.b.gemm_status_string(rc))
+
+    def plan(self):
+        return self.b.gemm_plan(0 if self.dtype == "int8" else 1, self.M, self.N, self.K, self.K, self.N,
+                                self.N, self.dA.data_ptr(), self.dBs[0].data_ptr(), self.dC.data_ptr())
+
+
+def time_workload(w: Workload, steps: int, warmup: int):
+    import torch
+    for _ in range(warmup):
+        w.launch()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record(w.stream)
+        w.launch()
+        ends[i].record(w.stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    return wall * 1e3 / steps, float(np.mean(kernel_ms)), float(np.min(kernel_ms))
+
+
+def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
+    ops = 2.0 * w.M * w.N * w.K
+    e = 1 if w.dtype == "int8" else 2
+    comp_bytes = w.M * w.K * e + w.K * w.N * e + w.M * w.N * 4
+    plan = w.plan()
+    value = ops / (ms_step * 1e-3) / 1e12
+    achieved = ops / (k_avg * 1e-3) / 1e12
+    mem_bound = ops / comp_bytes < (PEAK[w.dtype] * 1e12) / (HBM_GBS * 1e9)
+    traffic = traffic_for(w.dtype, w.M, w.N, w.K)
+    if mem_bound:
+        ach_gbs = comp_bytes / (k_avg * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach_gbs, 1), "peak": HBM_GBS, "unit": "GB/s",
+                "frac": round(ach_gbs / HBM_GBS, 4), "traffic": traffic}
+    else:
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK[w.dtype], "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK[w.dtype], 4), "traffic": traffic}
+    return {
+        "value": round(value, 2), "unit": "TOPS" if w.dtype == "int8" else "TFLOP/s",
+        "ms_per_step": round(ms_step, 5), "kernel_ms_avg": round(k_avg, 5), "kernel_ms_min": round(k_min, 5),
+        "pct_dense_peak": round(100.0 * value / PEAK[w.dtype], 2),
+        "plan": plan["name"], "split_k": plan["split_k"], "grid": plan["grid"],
+        "algorithmic_ops_per_launch": ops, "algorithmic_bytes_per_launch": comp_bytes,
+        "roofline": roof,
+    }
+
+
+def parity_sample(w: Workload, rows):
+    """Compares the timed output's sampled rows with the oracle (cheap evidence, not the test)."""
+    from oracle import oracle
+    o = oracle.get()
+    C = w.dC[rows].cpu().numpy()
+    Ar = np.ascontiguousarray(w.A_host[rows])
+    if w.dtype == "int8":
+        ref, ovf = o.gemm_i8_i32(Ar, w.B_host)
+        return bool(ovf == 0 and np.array_equal(C, ref))
+    from paper_2512_13282_amd import inputs
+    ref = o.gemm_bf16_f64(Ar, w.B_host)
+    err = oracle.normalized_error(C, ref, w.K, float(np.abs(inputs.f32_from_bf16_bits(w.A_host)).max()),
+                                  float(np.abs(inputs.f32_from_bf16_bits(w.B_host)).max()))
+    return bool(err <= 1e-5)
+
+
+def cpu_baseline(w: Workload, seconds: float):
+    """The oracle (as is) on the first rows of the same workload, sized to ~`seconds`."""
+    from oracle import oracle
+    o = oracle.get()
+    threads = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS")
+    if cap and cap.isdigit():
+        threads = min(threads, int(cap))
+    fn = o.gemm_i8_i32 if w.dtype == "int8" else o.gemm_bf16_f64
+    probe = max(1, min(w.M, threads))
+    t0 = time.perf_counter()
+    fn(np.ascontiguousarray(w.A_host[:probe]), w.B_host, nthreads=threads)
+    t_probe = time.perf_counter() - t0
+    rows = int(max(probe, min(w.M, probe * seconds / max(t_probe, 1e-6))))
+    rows = max(threads, (rows // threads) * threads) if rows >= threads else rows
+    t0 = time.perf_counter()
+    fn(np.ascontiguousarray(w.A_host[:rows]), w.B_host, nthreads=threads)
+    t = time.perf_counter() - t0
+    ops = 2.0 * rows * w.N * w.K
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(ops / t / 1e12, 6), "unit": "TOPS" if w.dtype == "int8" else "TFLOP/s",
+            "cores": threads, "kind": "oracle", "seconds": round(t, 3), "cpu_model": cpu,
+            "sample": f"first {rows} of {w.M} rows of C for the same {w.dtype} {w.M}x{w.K}x{w.N} GEMM "
+                      f"({rows * w.N} outputs, {ops:.3g} ops)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(GEMM shards by output tiles; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    from paper_2512_13282_amd import binding
+    binding.lib()   # fails loudly if the HIP library is not built
+
+    S = args.size
+    results = {}
+    for dtype in (["int8", "bf16"] if args.only is None else [args.only]):
+        w = Workload(dtype, S, S, S)
+        ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+        r = summarize(w, ms, kavg, kmin)
+        r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
+        if dtype == (args.only or "int8") and not args.no_cpu_baseline:
+            r["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        results[dtype] = (w, r)
+        print(f"[bench] {dtype} {S}^3: {r['value']} {r['unit']} ({r['pct_dense_peak']}% of dense peak), "
+              f"kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
+        del w
+
+    if args.sweep:
+        from paper_2512_13282_amd import inputs
+        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+        with open(os.path.join(ROOT, "gpurun_out", "sweep.jsonl"), "w") as f:
+            for (dtype, M, K, N) in inputs.ALL_CONFIGS:
+                e = 1 if dtype == "int8" else 2
+                bbytes = K * N * e
+                copies = 1 if M >= 256 else max(1, int(np.ceil(512e6 / bbytes)) + 1)
+                w = Workload(dtype, M, N, K, copies=copies)
+                ms, kavg, kmin = time_workload(w, max(20, args.steps // 2), args.warmup)
+                r = summarize(w, ms, kavg, kmin)
+                r.update({"dtype": dtype, "M": M, "K": K, "N": N, "b_copies": copies})
+                r["parity_sample_ok"] = parity_sample(w, sorted({0, M - 1}))
+                f.write(json.dumps(r) + "\n")
+                print(f"[sweep] {dtype:4s} M={M:5d} K={K:6d} N={N:6d} {r['value']:9.2f} {r['unit']:7s} "
+                      f"{r['pct_dense_peak']:6.2f}% kernel {r['kernel_ms_avg']*1e3:9.1f} us "
+                      f"{r['roofline']['bound']} frac={r['roofline']['frac']:.3f} plan={r['plan']} "
+                      f"split={r['split_k']} ok={r['parity_sample_ok']}", file=sys.stderr, flush=True)
+                del w
+                torch.cuda.empty_cache()
+
+    head_dtype = args.only or "int8"
+    hw, hr = results[head_dtype]
+    line = {
+        "metric": f"GEMM {'TOPS int8->int32' if head_dtype == 'int8' else 'TFLOP/s bf16->fp32'} "
+                  f"M=N=K={S} on 1 MI355X (% of dense MFMA peak in pct_dense_peak)",
+        "value": hr["value"], "unit": hr["unit"], "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": hr["ms_per_step"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "i8" if head_dtype == "int8" else "bf16",
+        "data": "synthetic: A, B seeded (PCG64 seed 0 / 1); int8 uniform [-128,127], bf16 N(0,1) rounded RNE",
+        "config": {"workload": f"{head_dtype} GEMM M=N=K={S}, row-major A, B, C "
+                               f"({'int32' if head_dtype == 'int8' else 'fp32'} output)",
+                   "M": S, "N": S, "K": S, "plan": hr["plan"], "split_k": hr["split_k"]},
+        "pct_dense_peak": hr["pct_dense_peak"],
+        "kernel_ms_avg": hr["kernel_ms_avg"],
+        "parity_sample_ok": hr["parity_sample_ok"],
+        "roofline": hr["roofline"],
+        "cpu_baseline": hr.get("cpu_baseline"),
+    }
+    for dtype, (w, r) in results.items():
+        if dtype != head_dtype:
+            line[dtype] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg", "pct_dense_peak",
+                                            "plan", "split_k", "parity_sample_ok", "roofline")}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

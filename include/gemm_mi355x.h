@@ -1,0 +1,136 @@
+/*
+ * gemm_mi355x.h -- C ABI of the MI355X (gfx950) dense GEMM library.
+ *
+ * Operation (paper, Sec. 4.1 "Multi-Level Tiling Method"): an M x K x N GEMM,
+ * C = A . B, with A the M x K input (typically activations), B the K x N input
+ * (typically weights) and C the M x N output.  Matrices stay in standard
+ * row-major order in memory with no pre-tiling (Sec. 1 and Sec. 4.3: the
+ * layout transformation into the tiled order the compute units need happens
+ * on the fly, inside the kernels), and arbitrary dimensions are supported
+ * (Sec. 5.3.1, where the paper zero-pads; here ragged tiles are masked, which
+ * gives the same result).
+ *
+ *   C[i*ldc + j] = sum_{k<K} A[i*lda + k] * B[k*ldb + j],  0 <= i < M, 0 <= j < N
+ *
+ * The result OVERWRITES C (no alpha/beta; the accumulator starts at zero as
+ * in the paper's output-stationary kernel, Sec. 4.2.1).  Elements of C outside
+ * the M x N window (row padding beyond N) are never touched.
+ *
+ * Layout: A, B and C are row-major; lda, ldb, ldc are row strides in ELEMENTS.
+ *
+ * Ownership: A, B and C are caller-owned DEVICE pointers on the current HIP
+ * device, valid until the work queued on `stream` has completed.  The library
+ * keeps no reference after a call returns.  The only memory it allocates is a
+ * split-K workspace taken with hipMallocAsync on `stream` and released with
+ * hipFreeAsync on the same stream (stream-ordered, so concurrent calls on
+ * different streams never share it).
+ *
+ * Execution: every GEMM call is asynchronous on `stream` (a hipStream_t passed
+ * as void*; NULL = the null stream) and never synchronizes the device.
+ *
+ * Errors: every entry point returns an int status (gemm_status_t) and never
+ * throws or aborts.  Argument checks run on the host BEFORE any HIP call:
+ *   GEMM_ERR_INVALID_VALUE  M, N or K < 0; lda < K (M, K > 0); ldb < N (K, N > 0);
+ *                           ldc < N (M, N > 0); a NULL pointer whose operand is
+ *                           non-empty; C overlapping A or B in memory.
+ *   GEMM_ERR_UNSUPPORTED    a forced plan (gemm_force_plan) that cannot run the
+ *                           given shape / alignment.
+ *   GEMM_ERR_NO_MEMORY      the split-K workspace could not be allocated.
+ *   GEMM_ERR_HIP            a HIP launch/runtime error.
+ * M == 0 or N == 0 is a successful no-op.  K == 0 writes zeros (empty sum).
+ * Pointers or strides that are not 16-byte aligned are accepted and routed to
+ * an alignment-agnostic kernel (slower, same result).
+ */
+#ifndef GEMM_MI355X_H
+#define GEMM_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GEMM_OK = 0,
+    GEMM_ERR_INVALID_VALUE = -1,
+    GEMM_ERR_UNSUPPORTED = -2,
+    GEMM_ERR_HIP = -3,
+    GEMM_ERR_NO_MEMORY = -4
+} gemm_status_t;
+
+typedef enum {
+    GEMM_DTYPE_I8_I32 = 0,   /* int8 inputs, exact int32 accumulate and output */
+    GEMM_DTYPE_BF16_F32 = 1  /* bf16 inputs, fp32 accumulate and output         */
+} gemm_dtype_t;
+
+/* Kernel families the selector chooses between (gemm_plan_info.kernel). */
+typedef enum {
+    GEMM_KERNEL_AUTO = -1,   /* gemm_force_plan: let the selector decide       */
+    GEMM_KERNEL_GENERIC = 0, /* any alignment; element-wise masked loads       */
+    GEMM_KERNEL_MACRO = 1,   /* 16-byte vector loads, large LDS macro-tiles    */
+    GEMM_KERNEL_SKINNY = 2   /* small M: narrow M tile, wide N, split-K        */
+} gemm_kernel_t;
+
+/* The selector's choice for one call (filled by gemm_plan). */
+typedef struct gemm_plan_info {
+    int32_t kernel;          /* gemm_kernel_t                                  */
+    int32_t config;          /* index of the tile configuration in the family  */
+    int32_t bm, bn, bk;      /* workgroup macro-tile (bk in elements)          */
+    int32_t waves;           /* wavefronts per workgroup                       */
+    int32_t mfma_m, mfma_n, mfma_k;  /* MFMA instruction shape                 */
+    int32_t split_k;         /* K slices (1 = no split)                        */
+    int64_t k_chunk;         /* K elements per slice                           */
+    int64_t grid;            /* workgroups of the main kernel                  */
+    int64_t lds_bytes;       /* LDS per workgroup                              */
+    int64_t workspace_bytes; /* split-K partials (0 when split_k == 1)         */
+    double  model_traffic_bytes; /* modelled global traffic: A and B re-reads
+                                    (A ~ MNK/BN, B ~ MNK/BM), C, partials      */
+    double  model_t_comp_us; /* modelled MFMA time at the plan's efficiency    */
+    double  model_t_mem_us;  /* modelled memory time at 8 TB/s                 */
+    char    name[48];        /* human-readable kernel/config name              */
+} gemm_plan_info;
+
+/* int8 x int8 -> int32.  Exact whenever every true sum fits in int32, which is
+ * guaranteed for K <= 131071 (|a*b| <= 2^14); beyond that results wrap modulo
+ * 2^32 as the hardware accumulator does. */
+int gemm_i8_i32(int64_t M, int64_t N, int64_t K,
+                const int8_t *A, int64_t lda,
+                const int8_t *B, int64_t ldb,
+                int32_t *C, int64_t ldc, void *stream);
+
+/* bf16 x bf16 -> fp32.  A and B hold raw bf16 bit patterns (uint16_t);
+ * products are exact and are accumulated in fp32 (order unspecified; split-K
+ * partials are summed in a fixed slice order, so results are run-to-run
+ * reproducible for a given plan). */
+int gemm_bf16_f32(int64_t M, int64_t N, int64_t K,
+                  const uint16_t *A, int64_t lda,
+                  const uint16_t *B, int64_t ldb,
+                  float *C, int64_t ldc, void *stream);
+
+/* Pure host: the plan a GEMM call with these arguments would use (alignment
+ * is taken from the three addresses, which are never dereferenced).
+ * Returns GEMM_OK, GEMM_ERR_INVALID_VALUE or GEMM_ERR_UNSUPPORTED. */
+int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K,
+              int64_t lda, int64_t ldb, int64_t ldc,
+              uintptr_t a_addr, uintptr_t b_addr, uintptr_t c_addr,
+              gemm_plan_info *out);
+
+/* Test and benchmark hook: force the kernel family, tile configuration
+ * (-1 = selector's choice within the family) and split-K factor (0 = the
+ * selector's) for every later call of `dtype` in this process, or restore
+ * automatic selection with kernel = GEMM_KERNEL_AUTO.  Not thread-safe with
+ * respect to concurrent GEMM calls.  Returns GEMM_ERR_INVALID_VALUE for an
+ * unknown kernel/config or a split factor < 0. */
+int gemm_force_plan(int dtype, int kernel, int config, int split_k);
+
+/* Static description of the error code. */
+const char *gemm_status_string(int status);
+
+/* Library version string. */
+const char *gemm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GEMM_MI355X_H */

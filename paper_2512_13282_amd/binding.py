@@ -1,0 +1,160 @@
+"""Thin ctypes binding over libgemm_mi355x.so (argument marshalling only).
+
+The functions named like the C entry points (``gemm_i8_i32``, ``gemm_bf16_f32``,
+``gemm_plan``, ``gemm_force_plan``, ``gemm_status_string``, ``gemm_version``)
+take plain integers and device addresses exactly as the C ABI does.  The two
+torch helpers (``mm_i8_i32``, ``mm_bf16_f32``) only read ``data_ptr()``,
+strides and the current HIP stream of torch tensors and call the same entry
+points; every step of the GEMM runs in the library's kernels.  There is no
+fallback: if the library is missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libgemm_mi355x.so")
+
+GEMM_OK = 0
+GEMM_ERR_INVALID_VALUE = -1
+GEMM_ERR_UNSUPPORTED = -2
+GEMM_ERR_HIP = -3
+GEMM_ERR_NO_MEMORY = -4
+
+GEMM_DTYPE_I8_I32 = 0
+GEMM_DTYPE_BF16_F32 = 1
+
+GEMM_KERNEL_AUTO = -1
+GEMM_KERNEL_GENERIC = 0
+GEMM_KERNEL_MACRO = 1
+GEMM_KERNEL_SKINNY = 2
+
+EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_plan", "gemm_force_plan",
+            "gemm_status_string", "gemm_version")
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("kernel", ctypes.c_int32), ("config", ctypes.c_int32),
+        ("bm", ctypes.c_int32), ("bn", ctypes.c_int32), ("bk", ctypes.c_int32),
+        ("waves", ctypes.c_int32),
+        ("mfma_m", ctypes.c_int32), ("mfma_n", ctypes.c_int32), ("mfma_k", ctypes.c_int32),
+        ("split_k", ctypes.c_int32),
+        ("k_chunk", ctypes.c_int64), ("grid", ctypes.c_int64),
+        ("lds_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+        ("model_traffic_bytes", ctypes.c_double),
+        ("model_t_comp_us", ctypes.c_double), ("model_t_mem_us", ctypes.c_double),
+        ("name", ctypes.c_char * 48),
+    ]
+
+
+class GemmError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(gemm_status_string(status))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2512_13282_amd.build`")
+        l = ctypes.CDLL(LIB_PATH)
+        i64, p, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+        gemm_args = [i64, i64, i64, p, i64, p, i64, p, i64, p]
+        l.gemm_i8_i32.argtypes = gemm_args
+        l.gemm_i8_i32.restype = i32
+        l.gemm_bf16_f32.argtypes = gemm_args
+        l.gemm_bf16_f32.restype = i32
+        l.gemm_plan.argtypes = [i32, i64, i64, i64, i64, i64, i64, ctypes.c_size_t,
+                                ctypes.c_size_t, ctypes.c_size_t, ctypes.POINTER(PlanInfo)]
+        l.gemm_plan.restype = i32
+        l.gemm_force_plan.argtypes = [i32, i32, i32, i32]
+        l.gemm_force_plan.restype = i32
+        l.gemm_status_string.argtypes = [i32]
+        l.gemm_status_string.restype = ctypes.c_char_p
+        l.gemm_version.argtypes = []
+        l.gemm_version.restype = ctypes.c_char_p
+        _lib = l
+    return _lib
+
+
+# ---------------------------------------------------------------- raw C entry points
+def gemm_i8_i32(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
+    return lib().gemm_i8_i32(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, stream or None)
+
+
+def gemm_bf16_f32(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
+    return lib().gemm_bf16_f32(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, stream or None)
+
+
+def gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr=0, b_addr=0, c_addr=0) -> dict:
+    """The selector's plan as a dict; raises GemmError on a bad argument."""
+    info = PlanInfo()
+    rc = lib().gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr, ctypes.byref(info))
+    if rc != GEMM_OK:
+        raise GemmError(rc)
+    d = {f: getattr(info, f) for f, _ in PlanInfo._fields_}
+    d["name"] = info.name.decode()
+    return d
+
+
+def gemm_force_plan(dtype, kernel=GEMM_KERNEL_AUTO, config=-1, split_k=0) -> int:
+    return lib().gemm_force_plan(dtype, kernel, config, split_k)
+
+
+def gemm_status_string(status: int) -> str:
+    return lib().gemm_status_string(status).decode()
+
+
+def gemm_version() -> str:
+    return lib().gemm_version().decode()
+
+
+# ---------------------------------------------------------------- torch helpers
+def _check(rc: int) -> None:
+    if rc != GEMM_OK:
+        raise GemmError(rc)
+
+
+def _mm(fn, A, B, out, in_dtype, out_dtype):
+    import torch
+    if A.dtype != in_dtype or B.dtype != in_dtype:
+        raise TypeError(f"expected {in_dtype} operands")
+    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[0]:
+        raise ValueError("expected A (M x K) and B (K x N)")
+    if not (A.is_cuda and B.is_cuda) or A.device != B.device:
+        raise ValueError("operands must be on the same GPU")
+    if A.stride(1) != 1 or B.stride(1) != 1:
+        raise ValueError("operands must be row-major with unit column stride")
+    M, K = A.shape
+    N = B.shape[1]
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=A.device)
+    elif out.dtype != out_dtype or tuple(out.shape) != (M, N) or out.stride(1) != 1 or out.device != A.device:
+        raise ValueError("bad output tensor")
+    stream = torch.cuda.current_stream(A.device).cuda_stream
+    # A single-row matrix has no meaningful row stride; any value >= cols is valid.
+    lda = A.stride(0) if M > 1 else max(K, 1)
+    ldb = B.stride(0) if K > 1 else max(N, 1)
+    ldc = out.stride(0) if M > 1 else max(N, 1)
+    _check(fn(M, N, K, A.data_ptr(), lda, B.data_ptr(), ldb, out.data_ptr(), ldc, stream))
+    return out
+
+
+def mm_i8_i32(A, B, out=None):
+    """C = A @ B for int8 torch tensors on the GPU; int32 result."""
+    import torch
+    return _mm(gemm_i8_i32, A, B, out, torch.int8, torch.int32)
+
+
+def mm_bf16_f32(A, B, out=None):
+    """C = A @ B for bfloat16 torch tensors on the GPU; float32 result."""
+    import torch
+    return _mm(gemm_bf16_f32, A, B, out, torch.bfloat16, torch.float32)

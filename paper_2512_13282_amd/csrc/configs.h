@@ -1,0 +1,61 @@
+// configs.h -- the tile configurations compiled into the library.
+//
+// One table, read by the host-side selector (selector.cpp) and by the launch
+// code (gemm_launch.hip), which instantiates exactly these kernels.  Pure C++:
+// no HIP headers, so the selector builds and tests on a machine without a GPU.
+//
+// Tiling levels (paper, Sec. 4.1: instruction tile r x s x t -> per-core kernel
+// m_ct x k_ct x n_ct -> whole-array tile -> full GEMM): here the MFMA
+// instruction tile -> the wave tile -> the workgroup macro-tile BM x BK x BN
+// staged through LDS -> the grid of output tiles.  Each workgroup owns one
+// output tile and reduces K in time with the accumulators held in registers
+// (output-stationary, Sec. 4.2.1); split-K (several workgroups per tile, each
+// on a K slice) is only used where too few output tiles exist to fill the GPU.
+#pragma once
+
+#include <stdint.h>
+
+namespace gemm {
+
+enum Dtype : int32_t { DT_I8 = 0, DT_BF16 = 1 };
+
+enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2 };
+
+struct TileConfig {
+    int32_t family;
+    int32_t bm, bn;      // workgroup macro-tile (rows of C, cols of C)
+    int32_t wm, wn;      // waves along M and N (wave tile = bm/wm x bn/wn)
+    int32_t occupancy;   // workgroups resident per CU (LDS and register bound)
+    double  eff;         // fraction of MFMA peak one resident workgroup set sustains
+    const char *name;
+};
+
+// K depth of one LDS stage is 128 bytes for both dtypes: 64 bf16 or 128 int8
+// elements.  Every MFMA consumes 32 bytes of K per lane pair (bf16 32x32x16,
+// int8 32x32x32), so a stage is 4 MFMA k-steps.
+constexpr int32_t kStageKBytes = 128;
+
+// Family GENERIC: alignment-agnostic element-wise loads (any lda/ldb/K/N).
+// Family MACRO: 16-byte vector loads; large tiles.
+// Family SKINNY: same loaders, narrow M tile for M <= 64.
+constexpr TileConfig kConfigs[] = {
+    // family       bm   bn  wm wn occ  eff   name
+    {FAM_GENERIC,   64,  64, 2, 2, 2, 0.10, "generic_64x64_w4"},
+    {FAM_GENERIC,  128, 128, 2, 2, 1, 0.15, "generic_128x128_w4"},
+    {FAM_MACRO,    256, 256, 2, 2, 1, 0.80, "macro_256x256_w4"},
+    {FAM_MACRO,    128, 256, 2, 2, 1, 0.70, "macro_128x256_w4"},
+    {FAM_MACRO,    256, 128, 2, 2, 1, 0.70, "macro_256x128_w4"},
+    {FAM_MACRO,    128, 128, 2, 2, 2, 0.60, "macro_128x128_w4"},
+    {FAM_SKINNY,    32, 256, 1, 4, 2, 0.40, "skinny_32x256_w4"},
+    {FAM_SKINNY,    64, 256, 1, 4, 2, 0.45, "skinny_64x256_w4"},
+};
+constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
+
+// LDS bytes of one workgroup: A (bm x 128 B) and B^T (bn x 128 B) stages,
+// double-buffered.  The analog of the paper's L1 budget (Eq. 5) without the C
+// term: the output tile lives in registers, not in LDS.
+constexpr int64_t lds_bytes(const TileConfig &c) {
+    return 2LL * (int64_t(c.bm) + int64_t(c.bn)) * kStageKBytes;
+}
+
+}  // namespace gemm

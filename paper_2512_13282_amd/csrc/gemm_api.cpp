@@ -1,0 +1,230 @@
+// gemm_api.cpp -- the C ABI entry points (host side).
+//
+// Validation happens here, on the host, before any HIP call; the plan comes
+// from the selector (cached per shape/alignment class); the launch goes
+// through launch_gemm (gemm_kernels.hip).
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <unordered_map>
+
+#include "../../include/gemm_mi355x.h"
+#include "configs.h"
+#include "launch.h"
+#include "selector.h"
+
+namespace {
+
+using gemm::Plan;
+using gemm::Problem;
+
+struct Override {
+    int32_t family = -1;   // -1 = automatic
+    int32_t config = -1;
+    int32_t split = 0;
+};
+
+std::mutex g_mu;
+Override g_override[2];
+
+struct Key {
+    int32_t dtype;
+    int64_t M, N, K;
+    bool vec;
+    bool operator==(const Key &o) const {
+        return dtype == o.dtype && M == o.M && N == o.N && K == o.K && vec == o.vec;
+    }
+};
+struct KeyHash {
+    size_t operator()(const Key &k) const {
+        uint64_t h = 1469598103934665603ULL;
+        auto mix = [&](uint64_t v) { h = (h ^ v) * 1099511628211ULL; };
+        mix(uint64_t(k.dtype)); mix(uint64_t(k.M)); mix(uint64_t(k.N)); mix(uint64_t(k.K));
+        mix(uint64_t(k.vec));
+        return size_t(h);
+    }
+};
+std::unordered_map<Key, Plan, KeyHash> g_cache;
+
+bool overlaps(uintptr_t a0, uint64_t alen, uintptr_t b0, uint64_t blen) {
+    if (alen == 0 || blen == 0) return false;
+    return a0 < b0 + blen && b0 < a0 + alen;
+}
+
+// Bytes spanned by a row-major rows x cols matrix with row stride ld.
+uint64_t span_bytes(int64_t rows, int64_t cols, int64_t ld, int64_t esize) {
+    if (rows <= 0 || cols <= 0) return 0;
+    return uint64_t((rows - 1) * ld + cols) * uint64_t(esize);
+}
+
+int validate(const Problem &p, const void *A, const void *B, const void *C) {
+    if (p.M < 0 || p.N < 0 || p.K < 0) return GEMM_ERR_INVALID_VALUE;
+    const int64_t e = gemm::elem_bytes(p.dtype);
+    const bool has_a = p.M > 0 && p.K > 0, has_b = p.K > 0 && p.N > 0, has_c = p.M > 0 && p.N > 0;
+    if (has_a && (A == nullptr || p.lda < p.K)) return GEMM_ERR_INVALID_VALUE;
+    if (has_b && (B == nullptr || p.ldb < p.N)) return GEMM_ERR_INVALID_VALUE;
+    if (has_c && (C == nullptr || p.ldc < p.N)) return GEMM_ERR_INVALID_VALUE;
+    // Natural alignment of the element types (a misaligned int32*/float*/bf16* is not a valid pointer).
+    if (has_a && (uintptr_t(A) % uintptr_t(e)) != 0) return GEMM_ERR_INVALID_VALUE;
+    if (has_b && (uintptr_t(B) % uintptr_t(e)) != 0) return GEMM_ERR_INVALID_VALUE;
+    if (has_c && (uintptr_t(C) % 4) != 0) return GEMM_ERR_INVALID_VALUE;
+    // Stride products must not overflow 64-bit byte offsets.
+    const int64_t lim = int64_t(1) << 55;
+    if (p.M > lim || p.N > lim || p.K > lim || (has_a && p.lda > lim / (p.M > 0 ? p.M : 1)) ||
+        (has_b && p.ldb > lim / (p.K > 0 ? p.K : 1)) || (has_c && p.ldc > lim / (p.M > 0 ? p.M : 1)))
+        return GEMM_ERR_INVALID_VALUE;
+    const uint64_t clen = span_bytes(p.M, p.N, p.ldc, 4);
+    if (has_c && has_a && overlaps(uintptr_t(C), clen, uintptr_t(A), span_bytes(p.M, p.K, p.lda, e)))
+        return GEMM_ERR_INVALID_VALUE;
+    if (has_c && has_b && overlaps(uintptr_t(C), clen, uintptr_t(B), span_bytes(p.K, p.N, p.ldb, e)))
+        return GEMM_ERR_INVALID_VALUE;
+    return GEMM_OK;
+}
+
+int plan_for(const Problem &p, Plan *out) {
+    Override ov;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        ov = g_override[p.dtype];
+    }
+    const bool forced = ov.family >= 0 || ov.config >= 0 || ov.split > 0;
+    if (!forced) {
+        const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p)};
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_cache.find(key);
+        if (it != g_cache.end()) {
+            *out = it->second;
+            return GEMM_OK;
+        }
+    }
+    Plan pl;
+    if (!gemm::select_plan(p, &pl, ov.family, ov.config, ov.split)) return GEMM_ERR_UNSUPPORTED;
+    if (!forced) {
+        const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p)};
+        std::lock_guard<std::mutex> lk(g_mu);
+        if (g_cache.size() > 4096) g_cache.clear();
+        g_cache.emplace(key, pl);
+    }
+    *out = pl;
+    return GEMM_OK;
+}
+
+int run(int32_t dtype, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+        int64_t ldb, void *C, int64_t ldc, void *stream) {
+    Problem p{dtype, M, N, K, lda, ldb, ldc, uintptr_t(A), uintptr_t(B), uintptr_t(C)};
+    int rc = validate(p, A, B, C);
+    if (rc != GEMM_OK) return rc;
+    if (M == 0 || N == 0) return GEMM_OK;
+    Plan pl;
+    rc = plan_for(p, &pl);
+    if (rc != GEMM_OK) return rc;
+
+    gemm::KernelArgs a{};
+    a.dtype = dtype;
+    a.A = A;
+    a.B = B;
+    a.C = C;
+    a.workspace = nullptr;
+    a.M = M; a.N = N; a.K = K;
+    a.lda = K > 0 ? lda : 0;
+    a.ldb = K > 0 ? ldb : 0;
+    a.ldc = ldc;
+    a.k_chunk = pl.k_chunk;
+    a.split_k = pl.split_k;
+    a.tiles_m = int32_t(pl.tiles_m);
+    a.tiles_n = int32_t(pl.tiles_n);
+    a.group_m = 4;
+    if (pl.grid > 0x7fffffff || pl.tiles_m > 0x7fffffff || pl.tiles_n > 0x7fffffff)
+        return GEMM_ERR_UNSUPPORTED;
+    const int lr = gemm::launch_gemm(a, pl.config, pl.grid, stream);
+    if (lr == gemm::LAUNCH_NO_MEMORY) return GEMM_ERR_NO_MEMORY;
+    if (lr != gemm::LAUNCH_OK) return GEMM_ERR_HIP;
+    return GEMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int gemm_i8_i32(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *B,
+                int64_t ldb, int32_t *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_I8, M, N, K, A, lda, B, ldb, C, ldc, stream);
+}
+
+int gemm_bf16_f32(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *B,
+                  int64_t ldb, float *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_BF16, M, N, K, A, lda, B, ldb, C, ldc, stream);
+}
+
+int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
+              uintptr_t a_addr, uintptr_t b_addr, uintptr_t c_addr, gemm_plan_info *out) {
+    if (out == nullptr || (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32))
+        return GEMM_ERR_INVALID_VALUE;
+    Problem p{dtype, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr};
+    int rc = validate(p, reinterpret_cast<const void *>(a_addr), reinterpret_cast<const void *>(b_addr),
+                      reinterpret_cast<const void *>(c_addr));
+    if (rc != GEMM_OK) return rc;
+    memset(out, 0, sizeof(*out));
+    if (M == 0 || N == 0) {
+        out->kernel = -1;
+        out->config = -1;
+        strncpy(out->name, "noop", sizeof(out->name) - 1);
+        return GEMM_OK;
+    }
+    Plan pl;
+    rc = plan_for(p, &pl);
+    if (rc != GEMM_OK) return rc;
+    const gemm::TileConfig &c = gemm::kConfigs[pl.config];
+    out->kernel = c.family;
+    out->config = pl.config;
+    out->bm = c.bm;
+    out->bn = c.bn;
+    out->bk = gemm::stage_k_elems(dtype);
+    out->waves = c.wm * c.wn;
+    out->mfma_m = 32;
+    out->mfma_n = 32;
+    out->mfma_k = dtype == GEMM_DTYPE_I8_I32 ? 32 : 16;
+    out->split_k = pl.split_k;
+    out->k_chunk = pl.k_chunk;
+    out->grid = pl.grid;
+    out->lds_bytes = gemm::lds_bytes(c);
+    out->workspace_bytes = pl.workspace_bytes;
+    out->model_traffic_bytes = pl.traffic_bytes;
+    out->model_t_comp_us = pl.t_comp_us;
+    out->model_t_mem_us = pl.t_mem_us;
+    strncpy(out->name, c.name, sizeof(out->name) - 1);
+    return GEMM_OK;
+}
+
+int gemm_force_plan(int dtype, int kernel, int config, int split_k) {
+    if (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32) return GEMM_ERR_INVALID_VALUE;
+    if (split_k < 0 || config < -1 || config >= gemm::kNumConfigs) return GEMM_ERR_INVALID_VALUE;
+    if (kernel < GEMM_KERNEL_AUTO || kernel > GEMM_KERNEL_SKINNY) return GEMM_ERR_INVALID_VALUE;
+    if (config >= 0 && kernel >= 0 && gemm::kConfigs[config].family != kernel) return GEMM_ERR_INVALID_VALUE;
+    std::lock_guard<std::mutex> lk(g_mu);
+    Override &o = g_override[dtype];
+    if (kernel == GEMM_KERNEL_AUTO && config < 0) {
+        o = Override{-1, -1, split_k};
+    } else {
+        o.family = kernel;
+        o.config = config;
+        o.split = split_k;
+    }
+    return GEMM_OK;
+}
+
+const char *gemm_status_string(int status) {
+    switch (status) {
+        case GEMM_OK: return "GEMM_OK: success";
+        case GEMM_ERR_INVALID_VALUE: return "GEMM_ERR_INVALID_VALUE: invalid argument";
+        case GEMM_ERR_UNSUPPORTED: return "GEMM_ERR_UNSUPPORTED: no kernel can run this plan";
+        case GEMM_ERR_HIP: return "GEMM_ERR_HIP: HIP launch or runtime error";
+        case GEMM_ERR_NO_MEMORY: return "GEMM_ERR_NO_MEMORY: split-K workspace allocation failed";
+        default: return "unknown gemm status";
+    }
+}
+
+const char *gemm_version(void) { return "gemm_mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,28 @@
+// launch.h -- interface between the host API (gemm_api.cpp) and the kernels.
+// Pure C++: no HIP types, so the API file builds without HIP headers.
+#pragma once
+
+#include <stdint.h>
+
+namespace gemm {
+
+struct KernelArgs {
+    int32_t dtype;                 // DT_I8 or DT_BF16
+    const void *A;
+    const void *B;
+    void *C;
+    void *workspace;               // split-K partials, set by launch_gemm
+    int64_t M, N, K;
+    int64_t lda, ldb, ldc;         // row strides in elements
+    int64_t k_chunk;               // K elements per slice
+    int32_t split_k;
+    int32_t tiles_m, tiles_n;      // output tiles along M and N
+    int32_t group_m;               // tile-rows per group in the launch order
+};
+
+enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2 };
+
+// Queues the plan's kernels on `stream` (a hipStream_t).  Never synchronizes.
+int launch_gemm(const KernelArgs &a, int32_t config, int64_t grid, void *stream);
+
+}  // namespace gemm

@@ -1,0 +1,117 @@
+// selector.cpp -- the paper's compute/memory balance model, transplanted.
+//
+// The paper picks its per-core tile by modelling compute time against data
+// movement time and searching for the point where the two balance
+// (Sec. 4.5.1, Eqs. 1-5; Sec. 4.5.2, Eqs. 6-10):
+//   * off-chip reads of A scale as M*K*N*ty(A) / (width of the output tile in N)
+//     and reads of B as M*K*N*ty(B) / (height in M) (Eqs. 6-7); C is written
+//     once (Eq. 8);
+//   * compute time is 2*M*K*N / (eff * peak) (Eq. 9), memory time is traffic /
+//     bandwidth (Eq. 10), and the better tile is the one with the smaller
+//     maximum of the two.
+// On the GPU the same two terms decide between macro-tiles, with two terms
+// the NPU does not have: wave quantization (output tiles are spread over 256
+// CUs in whole rounds) and split-K partial traffic, which the paper avoids by
+// never splitting K across cores (Sec. 4.2.1).  Split-K is therefore only
+// chosen where the tile count alone cannot fill the chip.
+#include "selector.h"
+
+#include <algorithm>
+#include <cmath>
+
+namespace gemm {
+
+int32_t elem_bytes(int32_t dtype) { return dtype == DT_I8 ? 1 : 2; }
+
+int32_t stage_k_elems(int32_t dtype) { return kStageKBytes / elem_bytes(dtype); }
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool vector_loads_ok(const Problem &p) {
+    const int64_t e = elem_bytes(p.dtype);
+    return (p.a_addr % 16 == 0) && (p.b_addr % 16 == 0) &&
+           ((p.lda * e) % 16 == 0) && ((p.ldb * e) % 16 == 0) &&
+           ((p.K * e) % 16 == 0) && (p.N % 8 == 0);
+}
+
+bool config_applicable(const Problem &p, int32_t cfg) {
+    if (cfg < 0 || cfg >= kNumConfigs) return false;
+    const TileConfig &c = kConfigs[cfg];
+    if (c.family == FAM_GENERIC) return true;
+    return vector_loads_ok(p);
+}
+
+Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip) {
+    const TileConfig &c = kConfigs[cfg];
+    const int64_t e = elem_bytes(p.dtype);
+    const int64_t bk = stage_k_elems(p.dtype);
+    Plan pl{};
+    pl.config = cfg;
+    pl.tiles_m = ceil_div(p.M, c.bm);
+    pl.tiles_n = ceil_div(p.N, c.bn);
+    const int64_t nkt = ceil_div(p.K, bk);  // K stages in total
+    if (p.K == 0) {
+        pl.split_k = 1;
+        pl.k_chunk = 0;
+    } else {
+        int64_t s = std::max<int64_t>(1, std::min<int64_t>(split, nkt));
+        pl.k_chunk = ceil_div(nkt, s) * bk;
+        pl.split_k = int32_t(ceil_div(p.K, pl.k_chunk));
+    }
+    pl.grid = pl.tiles_m * pl.tiles_n * pl.split_k;
+    pl.workspace_bytes = pl.split_k > 1 ? int64_t(pl.split_k) * p.M * p.N * 4 : 0;
+
+    // Compute: whole rounds of resident workgroups (wave quantization).
+    const double ops_clk = p.dtype == DT_I8 ? chip.i8_ops_per_clk_cu : chip.bf16_ops_per_clk_cu;
+    const double cu_rate = ops_clk * chip.clock_hz;                 // ops/s per CU
+    const int64_t slots = int64_t(chip.cus) * c.occupancy;
+    const int64_t rounds = ceil_div(pl.grid, slots);
+    const double wg_ops = 2.0 * c.bm * c.bn * double(pl.k_chunk);
+    const double wg_s = wg_ops / (cu_rate * c.eff / c.occupancy);
+    pl.t_comp_us = double(rounds) * wg_s * 1e6;
+
+    // Memory: compulsory traffic at HBM speed; tile re-reads (Eqs. 6-7 analog)
+    // mostly from L2/MALL; split-K partials written and read back once.
+    const double a_bytes = double(p.M) * p.K * e, b_bytes = double(p.K) * p.N * e;
+    const double c_bytes = double(p.M) * p.N * 4;
+    const double a_reads = a_bytes * double(pl.tiles_n);
+    const double b_reads = b_bytes * double(pl.tiles_m);
+    const double ws = pl.split_k > 1 ? 2.0 * double(pl.workspace_bytes) : 0.0;
+    pl.traffic_bytes = a_reads + b_reads + c_bytes + ws;
+    pl.t_mem_us = ((a_bytes + b_bytes + c_bytes + ws) / chip.hbm_bytes_per_s +
+                   (a_reads + b_reads - a_bytes - b_bytes) / chip.reread_bytes_per_s) * 1e6;
+
+    pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + chip.launch_us +
+                    (pl.split_k > 1 ? chip.launch_us : 0.0);
+    return pl;
+}
+
+bool select_plan(const Problem &p, Plan *out, int32_t forced_family, int32_t forced_config,
+                 int32_t forced_split, const Chip &chip) {
+    static const int32_t kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64};
+    bool found = false;
+    Plan best{};
+    for (int32_t cfg = 0; cfg < kNumConfigs; ++cfg) {
+        if (forced_config >= 0 && cfg != forced_config) continue;
+        if (forced_family >= 0 && kConfigs[cfg].family != forced_family) continue;
+        if (!config_applicable(p, cfg)) continue;
+        // The generic family only runs when nothing vectorised applies, or when forced.
+        if (forced_family < 0 && forced_config < 0 && kConfigs[cfg].family == FAM_GENERIC &&
+            vector_loads_ok(p))
+            continue;
+        for (int32_t s : kSplits) {
+            if (forced_split > 0 && s != 1) break;
+            const int32_t split = forced_split > 0 ? forced_split : s;
+            Plan pl = evaluate(p, cfg, split, chip);
+            if (forced_split <= 0 && pl.split_k != split) continue;   // duplicate of a smaller split
+            if (!found || pl.t_total_us < best.t_total_us * (1.0 - 1e-9)) {
+                best = pl;
+                found = true;
+            }
+        }
+    }
+    if (found) *out = best;
+    return found;
+}
+
+}  // namespace gemm

@@ -1,0 +1,57 @@
+// selector.h -- shape-driven choice of kernel, tile and split-K (host only).
+#pragma once
+
+#include <stdint.h>
+
+#include "configs.h"
+
+namespace gemm {
+
+struct Problem {
+    int32_t dtype;
+    int64_t M, N, K;
+    int64_t lda, ldb, ldc;
+    uintptr_t a_addr, b_addr, c_addr;
+};
+
+struct Plan {
+    int32_t config;      // index into kConfigs
+    int32_t split_k;     // >= 1
+    int64_t k_chunk;     // K elements per slice (multiple of the stage depth)
+    int64_t tiles_m, tiles_n;
+    int64_t grid;
+    int64_t workspace_bytes;
+    double  traffic_bytes, t_comp_us, t_mem_us, t_total_us;
+};
+
+// Chip constants used by the model (AMD's published MI355X figures).
+struct Chip {
+    int32_t cus = 256;              // 8 XCDs x 32 CUs
+    double  clock_hz = 2.4e9;
+    double  i8_ops_per_clk_cu = 8192.0;   // dense int8 MFMA
+    double  bf16_ops_per_clk_cu = 4096.0; // dense bf16 MFMA
+    double  hbm_bytes_per_s = 8.0e12;
+    double  reread_bytes_per_s = 16.0e12; // A/B tile re-reads mostly served by L2/MALL
+    double  launch_us = 2.0;              // per kernel launch on the stream
+};
+
+int32_t elem_bytes(int32_t dtype);
+int32_t stage_k_elems(int32_t dtype);    // K elements per 128-byte LDS stage
+
+// Whether the 16-byte vector loaders (MACRO / SKINNY) may run this problem.
+bool vector_loads_ok(const Problem &p);
+
+// Whether config `cfg` can run problem `p` at all.
+bool config_applicable(const Problem &p, int32_t cfg);
+
+// Evaluates the model for one (config, split) candidate.
+Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip = Chip());
+
+// Best plan under the model.  forced_family < 0 means any family; forced_config
+// >= 0 pins the configuration; forced_split > 0 pins the split factor.
+// Returns false if nothing applicable exists (only possible when forced).
+bool select_plan(const Problem &p, Plan *out, int32_t forced_family = -1,
+                 int32_t forced_config = -1, int32_t forced_split = 0,
+                 const Chip &chip = Chip());
+
+}  // namespace gemm

@@ -1,0 +1,242 @@
+"""GPU path vs the CPU oracle, through the C ABI (needs an MI355X).
+
+int8 -> int32 is compared element for element (bit-exact).  bf16 -> fp32 must
+satisfy max|C - C_ref| / (K * max|A| * max|B|) <= 1e-5, and on integer-valued
+bf16 operands (where every fp32 partial sum is exact in any order) it must be
+exact.  Full-size workloads are checked with Freivalds' test on the whole C
+plus oracle rows sampled one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2512_13282_amd import binding as b
+from paper_2512_13282_amd import inputs
+import gpu_helpers as g
+
+pytestmark = pytest.mark.gpu
+I8, BF = g.I8, g.BF
+NUM_CONFIGS = 8
+GENERIC_CONFIGS = (0, 1)
+
+
+@pytest.fixture(autouse=True)
+def _reset_plan():
+    g.unforce()
+    yield
+    g.unforce()
+
+
+def _inputs(dtype, M, N, K, seed):
+    return inputs.make_inputs("int8" if dtype == I8 else "bf16", M, N, K, seed=seed)
+
+
+def _check(dtype, A, B, C):
+    (g.check_i8 if dtype == I8 else g.check_bf16)(A, B, C)
+
+
+def test_native_library_is_the_path():
+    assert torch.cuda.is_available()
+    lib = b.lib()
+    maps = open("/proc/self/maps").read()
+    assert b.LIB_PATH in maps, "libgemm_mi355x.so is not mapped into this process"
+    assert "gfx950" in b.gemm_version()
+    assert lib is not None
+
+
+# Shapes every vectorised config accepts (K a multiple of 16 elements, N of 8),
+# ragged in M, N and K against every tile size.
+VEC_SHAPES = [(1, 8, 16), (37, 40, 48), (64, 256, 128), (300, 264, 1040), (257, 520, 2064),
+              (513, 776, 784)]
+# Shapes only the element-wise (generic) loaders accept.
+ODD_SHAPES = [(1, 1, 1), (3, 5, 7), (17, 13, 31), (65, 63, 129), (129, 255, 257), (70, 300, 1001)]
+
+
+@pytest.mark.parametrize("split", [1, 3])
+@pytest.mark.parametrize("config", range(NUM_CONFIGS))
+@pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
+def test_every_config_matches_oracle(dtype, config, split):
+    g.force(dtype, b.GEMM_KERNEL_AUTO, config, split)
+    for i, (M, N, K) in enumerate(VEC_SHAPES):
+        A, B = _inputs(dtype, M, N, K, seed=100 + i)
+        print(f"dtype={dtype} config={config} split={split} shape={(M, N, K)}", flush=True)
+        _check(dtype, A, B, g.gemm_gpu(dtype, A, B))
+    for i, (M, N, K) in enumerate(ODD_SHAPES):
+        A, B = _inputs(dtype, M, N, K, seed=200 + i)
+        if config in GENERIC_CONFIGS:
+            print(f"dtype={dtype} config={config} split={split} odd shape={(M, N, K)}", flush=True)
+            _check(dtype, A, B, g.gemm_gpu(dtype, A, B))
+        else:
+            dA, lda = g.to_dev(A)
+            dB, ldb = g.to_dev(B)
+            dC, ldc = g.out_buffer(M, N, dtype)
+            assert g.call(dtype, M, N, K, dA, lda, dB, ldb, dC, ldc) == b.GEMM_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("config", [0, 2, 3, 5, 6])
+def test_bf16_integer_valued_is_exact(config):
+    """Integer-valued bf16 in [-8, 8]: the fp32 result is exact whatever the order."""
+    M, N, K = 200, 264, 4096
+    A = inputs.small_int_bf16_matrix(M, K, seed=7)
+    B = inputs.small_int_bf16_matrix(K, N, seed=8)
+    for split in (1, 5):
+        g.force(BF, b.GEMM_KERNEL_AUTO, config, split)
+        C = g.gemm_gpu(BF, A, B)
+        ref = oracle.get().gemm_bf16_f64(A, B)
+        assert np.array_equal(C.astype(np.float64), ref), (config, split)
+
+
+@pytest.mark.parametrize("dtype,M,K,N", inputs.SMALL, ids=[f"{c[0]}-{c[1]}" for c in inputs.SMALL])
+def test_small_workloads_full_oracle(dtype, M, K, N):
+    d = I8 if dtype == "int8" else BF
+    A, B = inputs.make_inputs(dtype, M, N, K, seed=0)
+    _check(d, A, B, g.gemm_gpu(d, A, B))
+
+
+def _sampled_rows(M, seed=5):
+    rng = np.random.default_rng(seed)
+    rows = {0, M - 1, M // 2}
+    rows.update(int(x) for x in rng.integers(0, M, size=5))
+    return sorted(r for r in rows if 0 <= r < M)
+
+
+BIG = inputs.SQUARE + inputs.RECT + inputs.SKINNY
+
+
+@pytest.mark.parametrize("dtype,M,K,N", BIG, ids=[f"{c[0]}-{c[1]}x{c[2]}x{c[3]}" for c in BIG])
+def test_full_size_workloads(dtype, M, K, N):
+    """Full-size workload with the selector's plan (the configuration the benchmark times)."""
+    d = I8 if dtype == "int8" else BF
+    print(f"full-size {dtype} M={M} K={K} N={N} plan={b.gemm_plan(d, M, N, K, K, N, N)['name']}", flush=True)
+    A, B = inputs.make_inputs(dtype, M, N, K, seed=0)
+    C = g.gemm_gpu(d, A, B)
+    o = oracle.get()
+    rows = _sampled_rows(M)
+    Ar = np.ascontiguousarray(A[rows])
+    if d == I8:
+        assert o.freivalds_i8_i32(A, B, np.ascontiguousarray(C), trials=2) == 0
+        ref, ovf = o.gemm_i8_i32(Ar, B)
+        assert ovf == 0 and np.array_equal(C[rows], ref)
+    else:
+        ref = o.gemm_bf16_f64(Ar, B)
+        amax_a = float(np.max(np.abs(inputs.f32_from_bf16_bits(A))))
+        amax_b = float(np.max(np.abs(inputs.f32_from_bf16_bits(B))))
+        err = oracle.normalized_error(C[rows], ref, K, amax_a, amax_b)
+        assert err <= g.BF16_TOL, err
+        assert np.all(np.isfinite(C))
+
+
+@pytest.mark.parametrize("M,K,N", [(s[1], s[2], s[3]) for s in BIG if s[0] == "bf16"],
+                         ids=[f"{s[1]}x{s[2]}x{s[3]}" for s in BIG if s[0] == "bf16"])
+def test_full_size_bf16_integer_valued_freivalds(M, K, N):
+    """bf16 kernels at full size on integer-valued operands: the exact product, checked on
+    the whole C by Freivalds in exact integer arithmetic (values in [-8, 8] fit int8)."""
+    A = inputs.small_int_bf16_matrix(M, K, seed=11)
+    B = inputs.small_int_bf16_matrix(K, N, seed=12)
+    C = g.gemm_gpu(BF, A, B)
+    Ci = C.astype(np.int64)
+    assert np.array_equal(Ci.astype(np.float32), C), "non-integer output"
+    A8 = inputs.f32_from_bf16_bits(A).astype(np.int8)
+    B8 = inputs.f32_from_bf16_bits(B).astype(np.int8)
+    assert oracle.get().freivalds_i8_i32(A8, B8, np.ascontiguousarray(Ci.astype(np.int32)), trials=2) == 0
+
+
+@pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
+def test_k_zero_writes_zeros_and_keeps_padding(dtype):
+    M, N = 33, 40
+    dA, _ = g.to_dev(np.zeros((M, 1), np.int8 if dtype == I8 else np.uint16))
+    dB, _ = g.to_dev(np.zeros((1, N), np.int8 if dtype == I8 else np.uint16))
+    sentinel = 777 if dtype == I8 else 7.5
+    dC, ldc = g.out_buffer(M, N, dtype, pad_cols=5, sentinel=sentinel)
+    assert g.call(dtype, M, N, 0, dA, 1, dB, N, dC, ldc) == b.GEMM_OK
+    torch.cuda.synchronize()
+    host = dC.cpu().numpy()
+    C = host[: M * ldc].reshape(M, ldc)
+    assert (C[:, :N] == 0).all()
+    assert (C[:, N:] == sentinel).all() and (host[M * ldc:] == sentinel).all()
+
+
+@pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
+@pytest.mark.parametrize("pad,offs", [((16, 16, 16), (0, 0, 0)),      # aligned padding: vector path
+                                      ((3, 5, 7), (0, 0, 0)),         # odd strides: generic path
+                                      ((0, 0, 0), (1, 3, 0)),         # misaligned starts: generic
+                                      ((32, 8, 1), (16, 16, 0))])
+def test_strides_offsets_and_canaries(dtype, pad, offs):
+    M, N, K = 150, 136, 272
+    A, B = _inputs(dtype, M, N, K, seed=3)
+    dA, lda = g.to_dev(A, pad[0], offs[0])
+    dB, ldb = g.to_dev(B, pad[1], offs[1])
+    sentinel = -99 if dtype == I8 else -0.25
+    dC, ldc = g.out_buffer(M, N, dtype, pad[2], sentinel=sentinel)
+    assert g.call(dtype, M, N, K, dA, lda, dB, ldb, dC, ldc, offs[0], offs[1], 0) == b.GEMM_OK
+    torch.cuda.synchronize()
+    host = dC.cpu().numpy()
+    C = host[: M * ldc].reshape(M, ldc)
+    _check(dtype, A, B, np.ascontiguousarray(C[:, :N]))
+    assert (C[:, N:] == sentinel).all(), "row padding of C was written"
+    assert (host[M * ldc:] == sentinel).all(), "memory past C was written"
+
+
+def test_int8_split_k_is_invariant():
+    M, N, K = 96, 512, 4096
+    A, B = _inputs(I8, M, N, K, seed=9)
+    outs = []
+    for split in (1, 2, 5, 16, 32):
+        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split)
+        outs.append(g.gemm_gpu(I8, A, B))
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+    g.check_i8(A, B, outs[0])
+
+
+def test_bf16_split_k_is_reproducible():
+    M, N, K = 96, 512, 4096
+    A, B = _inputs(BF, M, N, K, seed=10)
+    g.force(BF, b.GEMM_KERNEL_AUTO, 6, 7)
+    c1 = g.gemm_gpu(BF, A, B)
+    c2 = g.gemm_gpu(BF, A, B)
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+    g.check_bf16(A, B, c1)
+
+
+@pytest.mark.parametrize("config", [2, 3, 6, 0])
+def test_int8_extremes_largest_k(config):
+    """(-128)(-128) over K = 14336 is 234,881,024, the largest sum of the workload sweep."""
+    g.force(I8, b.GEMM_KERNEL_AUTO, config, 0)
+    M, N, K = 64, 256, 14336
+    A = np.full((M, K), -128, np.int8)
+    B = np.full((K, N), -128, np.int8)
+    C = g.gemm_gpu(I8, A, B)
+    assert (C == 234881024).all()
+    B[:, ::2] = 127
+    C = g.gemm_gpu(I8, A, B)
+    assert (C[:, ::2] == -16256 * K).all() and (C[:, 1::2] == 234881024).all()
+
+
+def test_int8_wraps_past_int32():
+    """K = 131072 of (-128)(-128) = 2^31: documented to wrap modulo 2^32, like the oracle."""
+    M, N, K = 32, 64, 131072
+    A = np.full((M, K), -128, np.int8)
+    B = np.full((K, N), -128, np.int8)
+    for split in (1, 4):
+        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split)
+        C = g.gemm_gpu(I8, A, B)
+        ref, ovf = oracle.get().gemm_i8_i32(A[:1], B[:, :1])
+        assert ovf == 1
+        assert (C == ref[0, 0]).all(), (split, np.unique(C)[:4])
+
+
+def test_torch_helpers():
+    M, N, K = 130, 264, 520
+    A, B = inputs.make_inputs("int8", M, N, K, seed=1)
+    tA, tB = torch.from_numpy(A).to(g.DEV), torch.from_numpy(B).to(g.DEV)
+    C = b.mm_i8_i32(tA, tB)
+    g.check_i8(A, B, C.cpu().numpy())
+    A, B = inputs.make_inputs("bf16", M, N, K, seed=2)
+    tA = torch.from_numpy(A.view(np.int16)).to(g.DEV).view(torch.bfloat16)
+    tB = torch.from_numpy(B.view(np.int16)).to(g.DEV).view(torch.bfloat16)
+    C = b.mm_bf16_f32(tA, tB)
+    g.check_bf16(A, B, C.cpu().numpy())
+    with pytest.raises(TypeError):
+        b.mm_i8_i32(tA, tB)

@@ -1,0 +1,115 @@
+"""The shape-driven selector (pure host code, exercised through gemm_plan)."""
+import itertools
+
+import pytest
+
+from paper_2512_13282_amd import binding as b
+from paper_2512_13282_amd import inputs
+
+I8, BF = b.GEMM_DTYPE_I8_I32, b.GEMM_DTYPE_BF16_F32
+DT = {"int8": I8, "bf16": BF}
+ESZ = {I8: 1, BF: 2}
+AL = 1 << 40    # 16-byte aligned fake addresses, far apart (never dereferenced)
+LDS_MAX = 160 * 1024
+
+
+def plan(dtype, M, N, K, lda=None, ldb=None, ldc=None, off=0):
+    return b.gemm_plan(dtype, M, N, K, lda or max(K, 1), ldb or max(N, 1), ldc or max(N, 1),
+                       AL + off, 2 * AL, 3 * AL)
+
+
+def check_invariants(p, dtype, M, N, K):
+    stage = 128 // ESZ[dtype]
+    assert p["lds_bytes"] <= LDS_MAX
+    assert p["bk"] == stage
+    tiles_m = -(-M // p["bm"])
+    tiles_n = -(-N // p["bn"])
+    assert p["grid"] == tiles_m * tiles_n * p["split_k"]
+    if K > 0:
+        assert p["k_chunk"] % stage == 0 and p["k_chunk"] > 0
+        assert p["split_k"] * p["k_chunk"] >= K > (p["split_k"] - 1) * p["k_chunk"]
+    else:
+        assert p["split_k"] == 1
+    assert p["workspace_bytes"] == (p["split_k"] * M * N * 4 if p["split_k"] > 1 else 0)
+    assert p["grid"] < 2 ** 31
+
+
+SIZES = [1, 2, 3, 15, 16, 17, 31, 33, 63, 64, 65, 127, 129, 255, 257, 1000, 4096]
+
+
+@pytest.mark.parametrize("dtype", [I8, BF])
+def test_every_shape_gets_a_valid_plan(dtype):
+    for M, N, K in itertools.product([1, 17, 64, 257, 4096], [1, 8, 33, 256, 4000], [0, 1, 16, 100, 8192]):
+        p = plan(dtype, M, N, K)
+        check_invariants(p, dtype, M, N, K)
+
+
+@pytest.mark.parametrize("dtype", [I8, BF])
+def test_alignment_routes_to_generic(dtype):
+    # K not a multiple of the 16-byte chunk -> element-wise loaders
+    p = plan(dtype, 512, 512, 4096 + 1)
+    assert p["kernel"] == b.GEMM_KERNEL_GENERIC
+    # misaligned A pointer -> generic
+    p = plan(dtype, 512, 512, 4096, off=ESZ[dtype])
+    assert p["kernel"] == b.GEMM_KERNEL_GENERIC
+    # N not a multiple of 8 -> generic
+    p = plan(dtype, 512, 4100, 4096)
+    assert p["kernel"] == b.GEMM_KERNEL_GENERIC
+    # everything aligned -> vectorised family
+    p = plan(dtype, 512, 512, 4096)
+    assert p["kernel"] in (b.GEMM_KERNEL_MACRO, b.GEMM_KERNEL_SKINNY)
+
+
+@pytest.mark.parametrize("dtype", ["int8", "bf16"])
+def test_workload_plans(dtype):
+    d = DT[dtype]
+    big = plan(d, 8192, 8192, 8192)
+    assert big["name"] == "macro_256x256_w4" and big["split_k"] == 1
+    for (_, M, K, N) in [c for c in inputs.ALL_CONFIGS if c[0] == dtype]:
+        p = plan(d, M, N, K)
+        check_invariants(p, d, M, N, K)
+        assert p["kernel"] != b.GEMM_KERNEL_GENERIC
+
+
+def test_skinny_shapes_split_k():
+    for d in (I8, BF):
+        p = plan(d, 16, 4096, 14336)
+        assert p["split_k"] > 1
+        assert p["bm"] <= 64
+
+
+def test_forced_plans():
+    try:
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_GENERIC, -1, 3) == b.GEMM_OK
+        p = plan(I8, 300, 200, 1000)
+        assert p["kernel"] == b.GEMM_KERNEL_GENERIC and p["split_k"] == 3
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_MACRO, 2, 1) == b.GEMM_OK
+        p = plan(I8, 300, 256, 1024)
+        assert p["config"] == 2 and p["split_k"] == 1
+        # a forced vectorised plan cannot run misaligned K
+        with pytest.raises(b.GemmError) as e:
+            plan(I8, 300, 256, 1001)
+        assert e.value.status == b.GEMM_ERR_UNSUPPORTED
+        # split larger than the number of stages is clamped
+        assert b.gemm_force_plan(BF, b.GEMM_KERNEL_AUTO, -1, 64) == b.GEMM_OK
+        p = plan(BF, 64, 64, 128)
+        assert p["split_k"] == 2
+    finally:
+        b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
+        b.gemm_force_plan(BF, b.GEMM_KERNEL_AUTO, -1, 0)
+
+
+def test_traffic_model_follows_eqs_6_to_8():
+    # A reads scale with the number of N tiles, B reads with the number of M tiles (Eqs. 6-7),
+    # C is written once (Eq. 8); no split -> no partial traffic.
+    M = N = K = 8192
+    p = plan(I8, M, N, K)
+    tiles_m, tiles_n = M // p["bm"], N // p["bn"]
+    expect = M * K * tiles_n + K * N * tiles_m + M * N * 4
+    assert abs(p["model_traffic_bytes"] - expect) < 1e-6 * expect
+
+
+def test_plans_are_deterministic():
+    a = plan(BF, 2048, 11008, 4096)
+    c = plan(BF, 2048, 11008, 4096)
+    assert a == c
