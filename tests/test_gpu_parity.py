@@ -45,10 +45,10 @@ def test_native_library_is_the_path():
     assert lib is not None
 
 
-# Shapes every vectorised config accepts (K a multiple of 16 elements, N of 8),
-# ragged in M, N and K against every tile size.
-VEC_SHAPES = [(1, 8, 16), (37, 40, 48), (64, 256, 128), (300, 264, 1040), (257, 520, 2064),
-              (513, 776, 784)]
+# Shapes every vectorised config accepts (row strides K and N a multiple of 16
+# bytes for both dtypes), ragged in M, N and K against every tile size.
+VEC_SHAPES = [(1, 16, 16), (37, 48, 48), (64, 256, 128), (300, 272, 1040), (257, 528, 2064),
+              (513, 784, 784)]
 # Shapes only the element-wise (generic) loaders accept.
 ODD_SHAPES = [(1, 1, 1), (3, 5, 7), (17, 13, 31), (65, 63, 129), (129, 255, 257), (70, 300, 1001)]
 
@@ -108,7 +108,9 @@ BIG = inputs.SQUARE + inputs.RECT + inputs.SKINNY
 def test_full_size_workloads(dtype, M, K, N):
     """Full-size workload with the selector's plan (the configuration the benchmark times)."""
     d = I8 if dtype == "int8" else BF
-    print(f"full-size {dtype} M={M} K={K} N={N} plan={b.gemm_plan(d, M, N, K, K, N, N)['name']}", flush=True)
+    fake = 1 << 40   # plan only: addresses are never dereferenced
+    plan = b.gemm_plan(d, M, N, K, K, N, N, fake, 2 * fake, 3 * fake)
+    print(f"full-size {dtype} M={M} K={K} N={N} plan={plan['name']} split={plan['split_k']}", flush=True)
     A, B = inputs.make_inputs(dtype, M, N, K, seed=0)
     C = g.gemm_gpu(d, A, B)
     o = oracle.get()
