@@ -32,6 +32,7 @@ PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (A
 HBM_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2512_13282_amd", "csrc", "gemm_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+COPY_PROBE_BYTES = 512 * 1024 * 1024
 
 
 def parse():
@@ -44,6 +45,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--only", choices=["int8", "bf16"], default=None)
+    ap.add_argument("--config", type=int, default=-1,
+                    help="force one tile configuration (index into the library's table)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 512 MiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -198,6 +203,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     from paper_2512_13282_amd import binding
     binding.lib()   # fails loudly if the HIP library is not built
+    if args.config >= 0:
+        for d in (binding.GEMM_DTYPE_I8_I32, binding.GEMM_DTYPE_BF16_F32):
+            if binding.gemm_force_plan(d, binding.GEMM_KERNEL_AUTO, args.config, 0) != 0:
+                sys.exit(f"cannot force config {args.config}")
 
     S = args.size
     results = {}
@@ -212,6 +221,16 @@ def main():
         print(f"[bench] {dtype} {S}^3: {r['value']} {r['unit']} ({r['pct_dense_peak']}% of dense peak), "
               f"kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
         del w
+
+    if args.copy_probe:
+        # Elementwise copy of 512 MiB: reads 512 MiB, writes 512 MiB.  Profiled beside the
+        # GEMM so FETCH_SIZE / WRITE_SIZE can be scaled by what they read for known traffic.
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     if args.sweep:
         from paper_2512_13282_amd import inputs

@@ -68,7 +68,8 @@ typedef enum {
     GEMM_KERNEL_AUTO = -1,   /* gemm_force_plan: let the selector decide       */
     GEMM_KERNEL_GENERIC = 0, /* any alignment; element-wise masked loads       */
     GEMM_KERNEL_MACRO = 1,   /* 16-byte vector loads, large LDS macro-tiles    */
-    GEMM_KERNEL_SKINNY = 2   /* small M: narrow M tile, wide N, split-K        */
+    GEMM_KERNEL_SKINNY = 2,  /* small M: narrow M tile, wide N, split-K        */
+    GEMM_KERNEL_DIRECT = 3   /* global -> LDS direct loads, LDS transpose reads */
 } gemm_kernel_t;
 
 /* The selector's choice for one call (filled by gemm_plan). */

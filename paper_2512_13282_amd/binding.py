@@ -29,6 +29,7 @@ GEMM_KERNEL_AUTO = -1
 GEMM_KERNEL_GENERIC = 0
 GEMM_KERNEL_MACRO = 1
 GEMM_KERNEL_SKINNY = 2
+GEMM_KERNEL_DIRECT = 3
 
 EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_plan", "gemm_force_plan",
             "gemm_status_string", "gemm_version")

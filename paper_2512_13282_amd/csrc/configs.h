@@ -19,7 +19,7 @@ namespace gemm {
 
 enum Dtype : int32_t { DT_I8 = 0, DT_BF16 = 1 };
 
-enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2 };
+enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2, FAM_DIRECT = 3 };
 
 struct TileConfig {
     int32_t family;
@@ -38,6 +38,8 @@ constexpr int32_t kStageKBytes = 128;
 // Family GENERIC: alignment-agnostic element-wise loads (any lda/ldb/K/N).
 // Family MACRO: 16-byte vector loads; large tiles.
 // Family SKINNY: same loaders, narrow M tile for M <= 64.
+// Family DIRECT: both operands stream global -> LDS directly (buffer loads with
+// an LDS destination); B's fragments come from LDS transpose reads.
 constexpr TileConfig kConfigs[] = {
     // family       bm   bn  wm wn occ  eff   name
     {FAM_GENERIC,   64,  64, 2, 2, 2, 0.10, "generic_64x64_w4"},
@@ -48,6 +50,8 @@ constexpr TileConfig kConfigs[] = {
     {FAM_MACRO,    128, 128, 2, 2, 2, 0.60, "macro_128x128_w4"},
     {FAM_SKINNY,    32, 256, 1, 4, 2, 0.40, "skinny_32x256_w4"},
     {FAM_SKINNY,    64, 256, 1, 4, 2, 0.45, "skinny_64x256_w4"},
+    {FAM_DIRECT,   256, 256, 2, 2, 1, 0.85, "direct_256x256_w4"},
+    {FAM_DIRECT,   128, 256, 2, 2, 1, 0.75, "direct_128x256_w4"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

@@ -35,6 +35,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "configs.h"
 #include "launch.h"
 
@@ -145,6 +147,45 @@ __device__ __forceinline__ unsigned i8_col_dword(const u32x2_t (&rows)[N], int b
     const unsigned b2 = (rows[base + 4 * j + 2][c >> 2] >> sh) & 0xFFu;
     const unsigned b3 = (rows[base + 4 * j + 3][c >> 2] >> sh) & 0xFFu;
     return b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+}
+
+
+// v_perm_b32 byte select: selector byte values 0-3 pick bytes of the SECOND
+// operand, 4-7 bytes of the FIRST.
+__device__ __forceinline__ unsigned perm(unsigned hi, unsigned lo, unsigned sel) {
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// bf16 block: rows[base .. base+KPB) are row pieces of 8 columns (column c in
+// dword c/2, half c%2).  col[c][j] = (row 2j, row 2j+1) of column c.
+template <int KPB, int N>
+__device__ __forceinline__ void bf16_transpose(const u32x4_t (&rows)[N], int base, unsigned (&col)[8][KPB / 2]) {
+#pragma unroll
+    for (int j = 0; j < KPB / 2; ++j)
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            col[c][j] = perm(rows[base + 2 * j + 1][c >> 1], rows[base + 2 * j][c >> 1],
+                             (c & 1) ? 0x07060302u : 0x05040100u);
+}
+
+// int8 block: row pieces of 8 columns (column c in dword c/4, byte c%4).
+// col[c][j] = bytes (row 4j, 4j+1, 4j+2, 4j+3) of column c: pairs of rows are
+// interleaved bytewise first, then pairs of pairs halfword-wise.
+template <int KPB, int N>
+__device__ __forceinline__ void i8_transpose(const u32x2_t (&rows)[N], int base, unsigned (&col)[8][KPB / 4]) {
+#pragma unroll
+    for (int j = 0; j < KPB / 4; ++j)
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+            const unsigned r0 = rows[base + 4 * j + 0][d], r1 = rows[base + 4 * j + 1][d];
+            const unsigned r2 = rows[base + 4 * j + 2][d], r3 = rows[base + 4 * j + 3][d];
+            const unsigned lo01 = perm(r1, r0, 0x05010400u), hi01 = perm(r1, r0, 0x07030602u);
+            const unsigned lo23 = perm(r3, r2, 0x05010400u), hi23 = perm(r3, r2, 0x07030602u);
+            col[4 * d + 0][j] = perm(lo23, lo01, 0x05040100u);
+            col[4 * d + 1][j] = perm(lo23, lo01, 0x07060302u);
+            col[4 * d + 2][j] = perm(hi23, hi01, 0x05040100u);
+            col[4 * d + 3][j] = perm(hi23, hi01, 0x07060302u);
+        }
 }
 
 template <int DT, int BM, int BN, int WM, int WN, bool VEC, int WAVES_PER_EU>
@@ -376,6 +417,522 @@ void gemm_tile_kernel(KernelArgs args) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Vectorised kernel: 16-byte (A, bf16 B) and 8-byte (int8 B) buffer loads.
+//
+// Every global load goes through a buffer resource.  A load whose offset is
+// at or past the resource's size returns zero without touching memory, which
+// replaces all bounds branches: rows past M and columns past N get an offset
+// that is out of range by construction, the K tail of A is masked per chunk,
+// and the K tail of B (and every stage past the end of the slice) is masked
+// by shrinking the resource's size to the valid rows of the stage.  The loop
+// body is therefore branch-free, so loads, LDS traffic and MFMAs of one stage
+// live in one scheduling region.
+// ---------------------------------------------------------------------------
+
+// ---------------------------------------------------------------------------
+// Instruction interleaving inside one K stage.  Left alone, the scheduler
+// issues a stage's MFMAs back to back and leaves the B transposes, LDS
+// writes and next-stage loads as a serial tail before the barrier; with one
+// wave per SIMD nothing hides that tail.  These scheduling groups ask for one
+// MFMA per slot with the other work spread evenly between them, so it issues
+// while the matrix pipe is busy.
+// ---------------------------------------------------------------------------
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
+
+// true in exactly `n` of the `slots` positions, evenly spread
+constexpr bool spread(int m, int n, int slots) { return (m * n) / slots != ((m + 1) * n) / slots; }
+constexpr int share(int m, int n, int slots) { return ((m + 1) * n) / slots - (m * n) / slots; }
+
+template <int NMFMA, int NDSR, int NDSW, int NVMEM, int NVALU>
+__device__ __forceinline__ void interleave_stage() {
+    static_for<0, NMFMA>([&](auto mi) {
+        constexpr int m = decltype(mi)::value;
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                      // MFMA
+        if constexpr (spread(m, NVMEM, NMFMA)) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+        if constexpr (spread(m, NDSR, NMFMA)) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+        if constexpr (share(m, NVALU, NMFMA) > 0)
+            __builtin_amdgcn_sched_group_barrier(0x002, share(m, NVALU, NMFMA), 0);              // VALU
+        if constexpr (spread(m, NDSW, NMFMA)) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // DS write
+    });
+}
+
+constexpr int kBufferFlags = 0x00020000;   // raw untyped dword access (gfx9 family descriptor word 3)
+constexpr uint32_t kOOB = 0x80000000u;     // offset past any resource used here -> load returns 0
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint8_t *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(base), (short)0, (int)bytes, kBufferFlags);
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int WAVES_PER_EU>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
+                          amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+void gemm_vec_kernel(KernelArgs args) {
+    using T = TileKernel<DT, BM, BN, WM, WN, true>;
+    using acc_vec = typename Types<DT>::acc_vec;
+    using out_t = typename Types<DT>::out_t;
+    constexpr int E = T::E, BK = T::BK, VECE = T::VECE;
+    constexpr int TM = T::TM, TN = T::TN;
+    constexpr int THREADS = T::THREADS;
+    constexpr int KPB = T::KPB, OUTB = T::OUTB, B_BLOCKS = T::B_BLOCKS;
+    constexpr int A_CHUNKS = T::A_CHUNKS;
+
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (BM + BN) * kStageKBytes];
+    uint8_t *const a_lds = smem;
+    uint8_t *const b_lds = smem + 2 * BM * kStageKBytes;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wave_m = wave / WN, wave_n = wave % WN;
+
+    int tm, tn, slice;
+    map_tile(args, tm, tn, slice);
+    const int64_t M = args.M, N = args.N;
+    const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+    const int64_t k_begin = int64_t(slice) * args.k_chunk;
+    int64_t k_end = k_begin + args.k_chunk;
+    if (k_end > args.K) k_end = args.K;
+    const int nk = k_end > k_begin ? int((k_end - k_begin + BK - 1) / BK) : 0;
+    const int64_t lda_b = args.lda * E, ldb_b = args.ldb * E;   // row strides in bytes
+
+    // ---- per-thread global offsets (constant over the K loop) ----
+    // A: chunk i of this thread is row (i * THREADS + tid) / 8, logical chunk tid % 8.
+    // The per-chunk row step is uniform; rows at or past M are masked by the
+    // resource size (rows are contiguous with stride lda from the tile's first row).
+    const int a_c = tid & 7;
+    const uint32_t a_voff0 = uint32_t((tid >> 3) * lda_b + a_c * 16);
+    constexpr int A_ROW_STEP = THREADS / 8;
+    const int64_t a_rows_valid = (M - m0) < BM ? (M - m0) : BM;
+    const uint32_t a_bytes = uint32_t(a_rows_valid * lda_b);
+    // B: block bI of this thread covers k-rows kb*KPB .. +KPB and 8 columns from nb*8.
+    // Row r of the block is the uniform offset r * ldb_b.  Columns at or past N get an
+    // out-of-range base; K rows past the slice end are masked by the resource size
+    // (whole blocks, since the slice length is a multiple of KPB).
+    uint32_t b_voff[B_BLOCKS];
+#pragma unroll
+    for (int bI = 0; bI < B_BLOCKS; ++bI) {
+        const int b = bI * THREADS + tid;
+        const int nb = b % (BN / 8), kb = b / (BN / 8);
+        b_voff[bI] = (n0 + nb * 8 < N) ? uint32_t(kb * KPB * ldb_b + nb * 8 * E) : kOOB;
+    }
+    const uint8_t *const a_base = static_cast<const uint8_t *>(args.A) + (m0 * args.lda + k_begin) * E;
+    const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
+
+    // One stage of staged global data.
+    struct Stage {
+        u32x4_t a[A_CHUNKS];
+        u32x4_t b4[DT == DT_BF16 ? B_BLOCKS * KPB : 1];
+        u32x2_t b2[DT == DT_I8 ? B_BLOCKS * KPB : 1];
+    };
+
+    // Loads stage kt into st (kt may be past the last stage: every load then returns 0).
+    auto load_stage = [&](Stage &st, int kt) {
+        const int64_t rem = (k_end - k_begin) - int64_t(kt) * BK;   // valid K elements left
+        const __amdgpu_buffer_rsrc_t ra_rsrc = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
+        const uint32_t a0 = int64_t(a_c) * VECE < rem ? a_voff0 : kOOB;
+#pragma unroll
+        for (int i = 0; i < A_CHUNKS; ++i)
+            st.a[i] = __builtin_amdgcn_raw_buffer_load_b128(ra_rsrc, a0 + uint32_t(i * A_ROW_STEP * lda_b), 0, 0);
+        const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
+        const __amdgpu_buffer_rsrc_t rb_rsrc =
+            make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+#pragma unroll
+        for (int bI = 0; bI < B_BLOCKS; ++bI)
+#pragma unroll
+            for (int r = 0; r < KPB; ++r) {
+                const int soff = int(r * ldb_b);
+                if (DT == DT_BF16)
+                    st.b4[bI * KPB + r] = __builtin_amdgcn_raw_buffer_load_b128(rb_rsrc, b_voff[bI], soff, 0);
+                else
+                    st.b2[bI * KPB + r] = __builtin_amdgcn_raw_buffer_load_b64(rb_rsrc, b_voff[bI], soff, 0);
+            }
+    };
+
+    auto store_stage = [&](const Stage &st, int buf) {
+        uint8_t *const as = a_lds + buf * BM * kStageKBytes;
+        uint8_t *const bs = b_lds + buf * BN * kStageKBytes;
+#pragma unroll
+        for (int i = 0; i < A_CHUNKS; ++i) {
+            const int row = (i * THREADS + tid) >> 3;
+            *reinterpret_cast<u32x4_t *>(as + row * kStageKBytes + swz(a_c, row) * 16) = st.a[i];
+        }
+#pragma unroll
+        for (int bI = 0; bI < B_BLOCKS; ++bI) {
+            const int b = bI * THREADS + tid;
+            const int nb = b % (BN / 8), kb = b / (BN / 8);
+            const int byte = kb * OUTB;
+            const int chunk = byte >> 4, half = (byte >> 3) & 1;
+            const int base = bI * KPB;
+            constexpr int DW = OUTB / 4;                 // dwords per column piece
+            unsigned col[8][DW];
+            if (DT == DT_BF16) bf16_transpose<KPB>(st.b4, base, *reinterpret_cast<unsigned(*)[8][KPB / 2]>(&col));
+            else i8_transpose<KPB>(st.b2, base, *reinterpret_cast<unsigned(*)[8][KPB / 4]>(&col));
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const int n = nb * 8 + c;
+                uint8_t *dst = bs + n * kStageKBytes + swz(chunk, n) * 16 + half * 8;
+                if (DW == 4)
+                    *reinterpret_cast<u32x4_t *>(dst) = u32x4_t{col[c][0], col[c][DW > 1 ? 1 : 0],
+                                                                col[c][DW > 2 ? 2 : 0], col[c][DW > 3 ? 3 : 0]};
+                else
+                    *reinterpret_cast<u32x2_t *>(dst) = u32x2_t{col[c][0], col[c][DW > 1 ? 1 : 0]};
+            }
+        }
+    };
+
+    const int frag_row = lane & 31;
+    const int frag_half = lane >> 5;
+    const int wrow0 = wave_m * (BM / WM);
+    const int wcol0 = wave_n * (BN / WN);
+    u32x4_t fa[2][TM], fb[2][TN];
+    auto load_frags = [&](int buf, int s, int slot) {
+        const uint8_t *const as = a_lds + buf * BM * kStageKBytes;
+        const uint8_t *const bs = b_lds + buf * BN * kStageKBytes;
+        const int chunk = 2 * s + frag_half;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wrow0 + i * 32 + frag_row;
+            fa[slot][i] = *reinterpret_cast<const u32x4_t *>(as + row * kStageKBytes + swz(chunk, row) * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wcol0 + j * 32 + frag_row;
+            fb[slot][j] = *reinterpret_cast<const u32x4_t *>(bs + col * kStageKBytes + swz(chunk, col) * 16);
+        }
+    };
+
+    acc_vec acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = acc_vec{};
+
+    // MFMAs over the stage in LDS buffer `buf`; fragments of k-step s+1 are read
+    // while the MFMAs of k-step s run.  Expects k-step 0's fragments in slot 0.
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (s < 3) load_frags(buf, s + 1, (s + 1) & 1);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(fa[s & 1][i], fb[s & 1][j], acc[i][j]);
+        }
+    };
+
+    // Software pipeline, two stages of global loads in flight:
+    //   loop top (kt even): LDS[0] = stage kt, s1 = stage kt+1, s0 = stage kt+2 (in flight).
+    Stage s0, s1;
+    if (nk > 0) {
+        load_stage(s0, 0);
+        load_stage(s1, 1);
+        store_stage(s0, 0);
+        __syncthreads();
+        load_stage(s0, 2);
+        load_frags(0, 0, 0);
+    }
+    // Per-stage instruction counts for the interleave (per wave).
+    constexpr int N_MFMA = 4 * TM * TN;
+    constexpr int N_DSR = 3 * (TM + TN);                   // fragments of k-steps 1..3
+    constexpr int N_DSW = A_CHUNKS + B_BLOCKS * 8;
+    constexpr int N_VMEM = A_CHUNKS + B_BLOCKS * KPB;
+    constexpr int N_VALU = B_BLOCKS * 8 * (OUTB / 4) * (DT == DT_I8 ? 2 : 1) + N_VMEM + N_DSW;
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+        compute(0);
+        store_stage(s1, 1);
+        interleave_stage<N_MFMA, N_DSR, N_DSW, 0, N_VALU>();
+        __syncthreads();
+        load_stage(s1, kt + 3);
+        load_frags(1, 0, 0);
+        compute(1);
+        store_stage(s0, 0);
+        interleave_stage<N_MFMA, N_DSR + TM + TN, N_DSW, N_VMEM, N_VALU>();
+        __syncthreads();
+        load_stage(s0, kt + 4);
+        load_frags(0, 0, 0);
+    }
+    if (kt < nk) compute(0);
+
+    out_t *out;
+    int64_t ldo;
+    if (args.split_k > 1) {
+        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
+        ldo = N;
+    } else {
+        out = static_cast<out_t *>(args.C);
+        ldo = args.ldc;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Direct-to-LDS kernel (gfx950): both operands go from global memory straight
+// into LDS with buffer_load ... lds, and B's K-contiguous MFMA fragments are
+// produced by LDS transpose reads (ds_read_b64_tr_b16 / _b8) instead of an
+// in-register transpose.  The K loop then holds only loads, LDS reads, MFMAs
+// and one barrier per stage.
+//
+// LDS, per stage: A as BM rows of 128 K-bytes (16-byte chunks XOR-swizzled by
+// swz(c, row)), B untransposed as BK rows (k) of BN*E bytes (chunks swizzled by
+// a function of k mod 4 (bf16) or k mod 8 (int8), matched to the row sets the
+// transpose reads touch together).
+//
+// Transpose read, per 16-lane group (lane g within the group): every lane
+// supplies the address of one 8-byte piece; lane g receives column g of the
+// block formed by the group's pieces -- b16: 4 rows x 16 columns, lane g
+// addresses row g/4, columns 4(g%4)..+3; b8: 8 rows x 16 columns, lane g
+// addresses row g/2, columns 8(g%2)..+7.
+// ---------------------------------------------------------------------------
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+
+template <int DT> __device__ __forceinline__ int bswz(int k);
+template <> __device__ __forceinline__ int bswz<DT_BF16>(int k) {
+    const int m = k & 3;
+    return (m << 2) ^ ((m >> 1) << 1);          // 0, 4, 10, 14
+}
+template <> __device__ __forceinline__ int bswz<DT_I8>(int k) {
+    const int m = k & 7;
+    return (m << 1) | (m >> 2);                 // 0, 2, 4, 6, 9, 11, 13, 15
+}
+
+template <int DT> __device__ __forceinline__ u32x2_t lds_read_tr(const uint8_t *p);
+template <> __device__ __forceinline__ u32x2_t lds_read_tr<DT_BF16>(const uint8_t *p) {
+    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                                           (LDS_AS bf16x4_t *)(const_cast<uint8_t *>(p))));
+}
+template <> __device__ __forceinline__ u32x2_t lds_read_tr<DT_I8>(const uint8_t *p) {
+    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                                           (LDS_AS i32x2_t *)(const_cast<uint8_t *>(p))));
+}
+
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, uint8_t *lds_wave_base, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LDS_AS void *)lds_wave_base, 16, int(voff), 0, 0, 0);
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int WAVES_PER_EU>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
+                          amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
+void gemm_lds_kernel(KernelArgs args) {
+    using acc_vec = typename Types<DT>::acc_vec;
+    using out_t = typename Types<DT>::out_t;
+    constexpr int E = Types<DT>::E;
+    constexpr int VECE = 16 / E;
+    constexpr int BK = kStageKBytes / E;                  // K elements per stage
+    constexpr int THREADS = 64 * WM * WN;
+    constexpr int WAVES = WM * WN;
+    constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+    constexpr int A_STAGE = BM * kStageKBytes;            // bytes
+    constexpr int B_PITCH = BN * E;                       // bytes per B row in LDS
+    constexpr int B_STAGE = BK * B_PITCH;                 // == BN * 128
+    constexpr int A_INSTR = A_STAGE / 1024 / WAVES;       // 1 KiB per wave-wide load
+    constexpr int B_INSTR = B_STAGE / 1024 / WAVES;
+    constexpr int B_ROWS_PER_KB = 1024 / B_PITCH;         // B rows covered by one wave-wide load
+    static_assert(A_INSTR >= 1 && A_INSTR * 1024 * WAVES == A_STAGE, "A stage split");
+    static_assert(B_INSTR >= 1 && B_INSTR * 1024 * WAVES == B_STAGE, "B stage split");
+    static_assert(B_PITCH <= 1024 && 1024 % B_PITCH == 0, "B row pitch");
+
+    // One LDS array per stage buffer and operand: with every access naming a
+    // fixed array, the compiler can tell the direct-to-LDS writes of one stage
+    // from the fragment reads of the other and does not serialise them.
+    __shared__ __attribute__((aligned(1024))) uint8_t a_lds0[A_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t a_lds1[A_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t b_lds0[B_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t b_lds1[B_STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wave_m = wave / WN, wave_n = wave % WN;
+
+    int tm, tn, slice;
+    map_tile(args, tm, tn, slice);
+    const int64_t M = args.M, N = args.N;
+    const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+    const int64_t k_begin = int64_t(slice) * args.k_chunk;
+    int64_t k_end = k_begin + args.k_chunk;
+    if (k_end > args.K) k_end = args.K;
+    const int nk = k_end > k_begin ? int((k_end - k_begin + BK - 1) / BK) : 0;
+    const int64_t lda_b = args.lda * E, ldb_b = args.ldb * E;
+
+    // ---- global source offsets of this lane's 16-byte pieces (constant over K) ----
+    // A load i of this wave fills LDS bytes [(i*WAVES + wave) KiB, +1 KiB): lane L
+    // writes physical chunk L%8 of row (i*WAVES + wave)*8 + L/8, which holds the
+    // logical chunk c = (L%8) ^ f(row).
+    const int64_t a_rows_valid = (M - m0) < BM ? (M - m0) : BM;
+    const uint32_t a_bytes = uint32_t(a_rows_valid * lda_b);
+    uint32_t a_voff[A_INSTR];
+    int a_chunk[A_INSTR];
+#pragma unroll
+    for (int i = 0; i < A_INSTR; ++i) {
+        const int row = (i * WAVES + wave) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+        a_chunk[i] = c;
+        a_voff[i] = uint32_t(row * lda_b + c * 16);
+    }
+    // B load i fills LDS bytes [(i*WAVES + wave) KiB, +1 KiB) of the B stage: lane L
+    // writes physical chunk p = L % (B_PITCH/16) of row (i*WAVES+wave)*B_ROWS_PER_KB +
+    // L / (B_PITCH/16), holding logical chunk p ^ bswz(row).
+    constexpr int B_CPR = B_PITCH / 16;                   // chunks per B row
+    uint32_t b_voff[B_INSTR];
+#pragma unroll
+    for (int i = 0; i < B_INSTR; ++i) {
+        const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
+        const int c = (lane % B_CPR) ^ bswz<DT>(row);
+        b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
+    }
+    const uint8_t *const a_base = static_cast<const uint8_t *>(args.A) + (m0 * args.lda + k_begin) * E;
+    const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
+
+    // Issues the loads of stage kt into LDS buffer BUF (kt past the end: zeros).
+    auto load_stage = [&](int kt, auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const int64_t rem = (k_end - k_begin) - int64_t(kt) * BK;
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
+        uint8_t *const as = BUF ? a_lds1 : a_lds0;
+#pragma unroll
+        for (int i = 0; i < A_INSTR; ++i) {
+            const uint32_t off = int64_t(a_chunk[i]) * VECE < rem ? a_voff[i] : kOOB;
+            load_lds16(ra, as + (i * WAVES + wave) * 1024, off);
+        }
+        const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
+        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+        uint8_t *const bs = BUF ? b_lds1 : b_lds0;
+#pragma unroll
+        for (int i = 0; i < B_INSTR; ++i) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+    };
+
+    // ---- fragment addressing ----
+    const int frag_row = lane & 31;
+    const int frag_half = lane >> 5;
+    const int wrow0 = wave_m * (BM / WM);
+    const int wcol0 = wave_n * (BN / WN);
+    // B transpose reads: group = lane/16, g = lane%16.
+    const int grp = lane >> 4, g16 = lane & 15;
+    // bf16: rows 4*h + g/4 (+8 for the upper K half), columns 4*(g%4) (+16 for odd groups)
+    // int8: rows 8*h + g/2 (+16 for the upper K half), columns 8*(g%2) (+16 for odd groups)
+    constexpr int TR_ROWS = DT == DT_BF16 ? 4 : 8;        // rows per transpose read
+    const int tr_row = DT == DT_BF16 ? (g16 >> 2) : (g16 >> 1);
+    const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (grp & 1) * 32 * E / 2;
+    const int tr_khalf = (grp >> 1) * (DT == DT_BF16 ? 8 : 16);
+
+    u32x4_t fa[2][TM], fb[2][TN];
+    auto load_frags = [&](auto buf_c, int s, int slot) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const uint8_t *const as = BUF ? a_lds1 : a_lds0;
+        const uint8_t *const bs = BUF ? b_lds1 : b_lds0;
+        const int chunk = 2 * s + frag_half;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wrow0 + i * 32 + frag_row;
+            fa[slot][i] = *reinterpret_cast<const u32x4_t *>(as + row * kStageKBytes + swz(chunk, row) * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int colb = (wcol0 + j * 32) * E + tr_colb;          // byte column of this lane's piece
+            u32x2_t part[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int k = s * (32 / E) + tr_khalf + h * TR_ROWS + tr_row;
+                const int phys = (colb >> 4) ^ bswz<DT>(k);
+                part[h] = lds_read_tr<DT>(bs + k * B_PITCH + phys * 16 + (colb & 15));
+            }
+            fb[slot][j] = u32x4_t{part[0][0], part[0][1], part[1][0], part[1][1]};
+        }
+    };
+
+    acc_vec acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = acc_vec{};
+
+    auto compute = [&](auto buf_c) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if (s < 3) load_frags(buf_c, s + 1, (s + 1) & 1);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(fa[s & 1][i], fb[s & 1][j], acc[i][j]);
+        }
+    };
+
+    // Pipeline: stage kt+1 streams into the other LDS buffer while stage kt is
+    // consumed; each wave waits for its own loads, then the barrier publishes
+    // them to the workgroup and retires the buffer just read.  Unrolled by two
+    // so that every LDS access names its buffer statically.
+    constexpr std::integral_constant<int, 0> B0{};
+    constexpr std::integral_constant<int, 1> B1{};
+    if (nk > 0) {
+        load_stage(0, B0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        load_frags(B0, 0, 0);
+    }
+    // The scheduling fences keep each stage's loads at its start: left free, the
+    // scheduler sinks them to just before the wait that ends the stage.
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+        load_stage(kt + 1, B1);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(B0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        load_frags(B1, 0, 0);
+        load_stage(kt + 2, B0);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(B1);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        load_frags(B0, 0, 0);
+    }
+    if (kt < nk) compute(B0);
+
+    out_t *out;
+    int64_t ldo;
+    if (args.split_k > 1) {
+        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
+        ldo = N;
+    } else {
+        out = static_cast<out_t *>(args.C);
+        ldo = args.ldc;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
+            }
+        }
+    }
+}
+
 // Sums split-K partials [split][M][N] into C in slice order 0, 1, ... (a fixed
 // order, so fp32 results are reproducible run to run).
 template <typename T>
@@ -397,8 +954,19 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const T *__restrict_
 // ---------------------------------------------------------------------------
 template <int DT, int BM, int BN, int WM, int WN, bool VEC, int WPE>
 static hipError_t launch_tile(const KernelArgs &a, int64_t grid, hipStream_t stream) {
-    hipLaunchKernelGGL((gemm_tile_kernel<DT, BM, BN, WM, WN, VEC, WPE>), dim3(unsigned(grid)),
-                       dim3(64 * WM * WN), 0, stream, a);
+    if constexpr (VEC)
+        hipLaunchKernelGGL((gemm_vec_kernel<DT, BM, BN, WM, WN, WPE>), dim3(unsigned(grid)),
+                           dim3(64 * WM * WN), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_tile_kernel<DT, BM, BN, WM, WN, false, WPE>), dim3(unsigned(grid)),
+                           dim3(64 * WM * WN), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int WPE>
+static hipError_t launch_direct(const KernelArgs &a, int64_t grid, hipStream_t stream) {
+    hipLaunchKernelGGL((gemm_lds_kernel<DT, BM, BN, WM, WN, WPE>), dim3(unsigned(grid)), dim3(64 * WM * WN), 0,
+                       stream, a);
     return hipGetLastError();
 }
 
@@ -413,6 +981,8 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
         case 5: return launch_tile<DT, 128, 128, 2, 2, true, 2>(a, grid, s);
         case 6: return launch_tile<DT, 32, 256, 1, 4, true, 2>(a, grid, s);
         case 7: return launch_tile<DT, 64, 256, 1, 4, true, 2>(a, grid, s);
+        case 8: return launch_direct<DT, 256, 256, 2, 2, 1>(a, grid, s);
+        case 9: return launch_direct<DT, 128, 256, 2, 2, 1>(a, grid, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -28,10 +28,15 @@ int32_t stage_k_elems(int32_t dtype) { return kStageKBytes / elem_bytes(dtype); 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 bool vector_loads_ok(const Problem &p) {
+    // 16-byte pieces of A rows and B rows must start 16-byte aligned and never
+    // straddle the end of a row; buffer offsets are 32-bit, so a 256-row panel
+    // of either operand must span less than 2 GiB.
     const int64_t e = elem_bytes(p.dtype);
+    const int64_t max_row_bytes = int64_t(1) << 22;
     return (p.a_addr % 16 == 0) && (p.b_addr % 16 == 0) &&
            ((p.lda * e) % 16 == 0) && ((p.ldb * e) % 16 == 0) &&
-           ((p.K * e) % 16 == 0) && (p.N % 8 == 0);
+           ((p.K * e) % 16 == 0) && ((p.N * e) % 16 == 0) &&
+           p.lda * e <= max_row_bytes && p.ldb * e <= max_row_bytes;
 }
 
 bool config_applicable(const Problem &p, int32_t cfg) {

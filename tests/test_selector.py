@@ -57,14 +57,14 @@ def test_alignment_routes_to_generic(dtype):
     assert p["kernel"] == b.GEMM_KERNEL_GENERIC
     # everything aligned -> vectorised family
     p = plan(dtype, 512, 512, 4096)
-    assert p["kernel"] in (b.GEMM_KERNEL_MACRO, b.GEMM_KERNEL_SKINNY)
+    assert p["kernel"] in (b.GEMM_KERNEL_MACRO, b.GEMM_KERNEL_SKINNY, b.GEMM_KERNEL_DIRECT)
 
 
 @pytest.mark.parametrize("dtype", ["int8", "bf16"])
 def test_workload_plans(dtype):
     d = DT[dtype]
     big = plan(d, 8192, 8192, 8192)
-    assert big["name"] == "macro_256x256_w4" and big["split_k"] == 1
+    assert big["name"] in ("macro_256x256_w4", "direct_256x256_w4") and big["split_k"] == 1
     for (_, M, K, N) in [c for c in inputs.ALL_CONFIGS if c[0] == dtype]:
         p = plan(d, M, N, K)
         check_invariants(p, d, M, N, K)
