@@ -43,10 +43,13 @@ def parse():
     ap.add_argument("--size", type=int, default=8192)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--only", choices=["int8", "bf16"], default=None)
     ap.add_argument("--config", type=int, default=-1,
                     help="force one tile configuration (index into the library's table)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
+                    help="write profiles/traffic.json from two rocprofv3 --pmc counter CSVs "
+                         "(FETCH_SIZE, WRITE_SIZE) of a `bench.py --copy-probe` run, then exit")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 512 MiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -193,8 +196,68 @@ def cpu_baseline(w: Workload, seconds: float):
                       f"({rows * w.N} outputs, {ops:.3g} ops)"}
 
 
+def write_traffic(fetch_csv: str, write_csv: str) -> None:
+    """HBM bytes per launch of the timed GEMM kernels from rocprofv3 counter CSVs.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by the factor that
+    makes them read the known traffic of the plain 512 MiB copy profiled in the same
+    run (it reads 512 MiB and writes 512 MiB)."""
+    import csv
+    import collections
+
+    def per_kernel(path, counter):
+        vals = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return vals
+
+    def copy_probe(vals):
+        # The probe's elementwise launches: the fill of its source (reads nothing) and
+        # three copies; the copies are the launches within 10% of the largest value.
+        cand = [v for k, vs in vals.items() if "elementwise" in k for v in vs]
+        if not cand:
+            sys.exit("no copy-probe kernel in the counter CSV (run bench.py --copy-probe under rocprofv3)")
+        top = max(cand)
+        sel = [v for v in cand if v >= 0.9 * top]
+        return sum(sel) / len(sel)
+
+    fetch_v = per_kernel(fetch_csv, "FETCH_SIZE")
+    write_v = per_kernel(write_csv, "WRITE_SIZE")
+    f_scale = COPY_PROBE_BYTES / (copy_probe(fetch_v) * 1024.0)
+    w_scale = COPY_PROBE_BYTES / (copy_probe(write_v) * 1024.0)
+    fetch = {k: sum(v) / len(v) for k, v in fetch_v.items()}
+    write = {k: sum(v) / len(v) for k, v in write_v.items()}
+    S = 8192
+    workloads = {}
+    for k in fetch:
+        if "gemm::" not in k:
+            continue
+        dtype = "int8" if "<0," in k else "bf16"
+        e = 1 if dtype == "int8" else 2
+        comp = S * S * e * 2 + S * S * 4
+        fb = fetch[k] * 1024.0 * f_scale
+        wb = write.get(k, 0.0) * 1024.0 * w_scale
+        workloads[f"{dtype}_{S}x{S}x{S}"] = {
+            "kernel": k, "fetch_bytes": round(fb), "write_bytes": round(wb),
+            "bytes_per_launch": round(fb + wb), "algorithmic_bytes": comp,
+            "traffic_over_algorithmic": round((fb + wb) / comp, 3)}
+    out = {"kernel_source_sha256": kernel_sha(), "fetch_scale": round(f_scale, 4),
+           "write_scale": round(w_scale, 4), "copy_probe_bytes": COPY_PROBE_BYTES,
+           "counters": "rocprofv3 --pmc FETCH_SIZE / --pmc WRITE_SIZE, KiB per dispatch, averaged",
+           "workloads": workloads}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=2)
+        f.write("\n")
+    print(json.dumps(out, indent=2))
+
+
 def main():
     args = parse()
+    if args.traffic_from:
+        write_traffic(*args.traffic_from)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(GEMM shards by output tiles; see the design notes). Run with --gpus 1.", file=sys.stderr)

@@ -430,39 +430,6 @@ void gemm_tile_kernel(KernelArgs args) {
 // live in one scheduling region.
 // ---------------------------------------------------------------------------
 
-// ---------------------------------------------------------------------------
-// Instruction interleaving inside one K stage.  Left alone, the scheduler
-// issues a stage's MFMAs back to back and leaves the B transposes, LDS
-// writes and next-stage loads as a serial tail before the barrier; with one
-// wave per SIMD nothing hides that tail.  These scheduling groups ask for one
-// MFMA per slot with the other work spread evenly between them, so it issues
-// while the matrix pipe is busy.
-// ---------------------------------------------------------------------------
-template <int I, int N, typename F>
-__device__ __forceinline__ void static_for(F &&f) {
-    if constexpr (I < N) {
-        f(std::integral_constant<int, I>{});
-        static_for<I + 1, N>(f);
-    }
-}
-
-// true in exactly `n` of the `slots` positions, evenly spread
-constexpr bool spread(int m, int n, int slots) { return (m * n) / slots != ((m + 1) * n) / slots; }
-constexpr int share(int m, int n, int slots) { return ((m + 1) * n) / slots - (m * n) / slots; }
-
-template <int NMFMA, int NDSR, int NDSW, int NVMEM, int NVALU>
-__device__ __forceinline__ void interleave_stage() {
-    static_for<0, NMFMA>([&](auto mi) {
-        constexpr int m = decltype(mi)::value;
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                      // MFMA
-        if constexpr (spread(m, NVMEM, NMFMA)) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
-        if constexpr (spread(m, NDSR, NMFMA)) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-        if constexpr (share(m, NVALU, NMFMA) > 0)
-            __builtin_amdgcn_sched_group_barrier(0x002, share(m, NVALU, NMFMA), 0);              // VALU
-        if constexpr (spread(m, NDSW, NMFMA)) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // DS write
-    });
-}
-
 constexpr int kBufferFlags = 0x00020000;   // raw untyped dword access (gfx9 family descriptor word 3)
 constexpr uint32_t kOOB = 0x80000000u;     // offset past any resource used here -> load returns 0
 
@@ -638,23 +605,15 @@ void gemm_vec_kernel(KernelArgs args) {
         load_stage(s0, 2);
         load_frags(0, 0, 0);
     }
-    // Per-stage instruction counts for the interleave (per wave).
-    constexpr int N_MFMA = 4 * TM * TN;
-    constexpr int N_DSR = 3 * (TM + TN);                   // fragments of k-steps 1..3
-    constexpr int N_DSW = A_CHUNKS + B_BLOCKS * 8;
-    constexpr int N_VMEM = A_CHUNKS + B_BLOCKS * KPB;
-    constexpr int N_VALU = B_BLOCKS * 8 * (OUTB / 4) * (DT == DT_I8 ? 2 : 1) + N_VMEM + N_DSW;
     int kt = 0;
     for (; kt + 1 < nk; kt += 2) {
         compute(0);
         store_stage(s1, 1);
-        interleave_stage<N_MFMA, N_DSR, N_DSW, 0, N_VALU>();
         __syncthreads();
         load_stage(s1, kt + 3);
         load_frags(1, 0, 0);
         compute(1);
         store_stage(s0, 0);
-        interleave_stage<N_MFMA, N_DSR + TM + TN, N_DSW, N_VMEM, N_VALU>();
         __syncthreads();
         load_stage(s0, kt + 4);
         load_frags(0, 0, 0);
@@ -779,7 +738,8 @@ void gemm_lds_kernel(KernelArgs args) {
     // ---- global source offsets of this lane's 16-byte pieces (constant over K) ----
     // A load i of this wave fills LDS bytes [(i*WAVES + wave) KiB, +1 KiB): lane L
     // writes physical chunk L%8 of row (i*WAVES + wave)*8 + L/8, which holds the
-    // logical chunk c = (L%8) ^ f(row).
+    // logical chunk c = (L%8) ^ f(row).  Rows at or past M are masked by the
+    // resource size (rows_valid * lda bytes from the tile's first row).
     const int64_t a_rows_valid = (M - m0) < BM ? (M - m0) : BM;
     const uint32_t a_bytes = uint32_t(a_rows_valid * lda_b);
     uint32_t a_voff[A_INSTR];
@@ -792,9 +752,11 @@ void gemm_lds_kernel(KernelArgs args) {
         a_voff[i] = uint32_t(row * lda_b + c * 16);
     }
     // B load i fills LDS bytes [(i*WAVES + wave) KiB, +1 KiB) of the B stage: lane L
-    // writes physical chunk p = L % (B_PITCH/16) of row (i*WAVES+wave)*B_ROWS_PER_KB +
-    // L / (B_PITCH/16), holding logical chunk p ^ bswz(row).
+    // writes physical chunk p = L % B_CPR of row (i*WAVES+wave)*B_ROWS_PER_KB + L / B_CPR,
+    // holding logical chunk p ^ bswz(row).  Columns at or past N get an out-of-range
+    // offset; K rows past the slice end are masked by the resource size.
     constexpr int B_CPR = B_PITCH / 16;                   // chunks per B row
+    static_assert(B_CPR >= 16, "transpose-read swizzle needs rows of at least 16 chunks");
     uint32_t b_voff[B_INSTR];
 #pragma unroll
     for (int i = 0; i < B_INSTR; ++i) {
@@ -804,61 +766,86 @@ void gemm_lds_kernel(KernelArgs args) {
     }
     const uint8_t *const a_base = static_cast<const uint8_t *>(args.A) + (m0 * args.lda + k_begin) * E;
     const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
+    const int64_t k_len = k_end - k_begin;
 
-    // Issues the loads of stage kt into LDS buffer BUF (kt past the end: zeros).
+    // Issues the loads of stage kt into LDS buffer BUF.  Full stages use the
+    // precomputed offsets as they are; only a partial last stage (and stages past
+    // the end, which load nothing) pays for the per-chunk K mask.
     auto load_stage = [&](int kt, auto buf_c) {
         constexpr int BUF = decltype(buf_c)::value;
-        const int64_t rem = (k_end - k_begin) - int64_t(kt) * BK;
+        const int64_t rem = k_len - int64_t(kt) * BK;
         const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
-        uint8_t *const as = BUF ? a_lds1 : a_lds0;
-#pragma unroll
-        for (int i = 0; i < A_INSTR; ++i) {
-            const uint32_t off = int64_t(a_chunk[i]) * VECE < rem ? a_voff[i] : kOOB;
-            load_lds16(ra, as + (i * WAVES + wave) * 1024, off);
-        }
         const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
         const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+        uint8_t *const as = BUF ? a_lds1 : a_lds0;
         uint8_t *const bs = BUF ? b_lds1 : b_lds0;
+        if (rem >= BK) {
 #pragma unroll
-        for (int i = 0; i < B_INSTR; ++i) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+            for (int i = 0; i < A_INSTR; ++i) {
+                load_lds16(ra, as + (i * WAVES + wave) * 1024, a_voff[i]);
+                if (i < B_INSTR) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+            }
+#pragma unroll
+            for (int i = A_INSTR; i < B_INSTR; ++i) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < A_INSTR; ++i) {
+                const uint32_t off = int64_t(a_chunk[i]) * VECE < rem ? a_voff[i] : kOOB;
+                load_lds16(ra, as + (i * WAVES + wave) * 1024, off);
+            }
+#pragma unroll
+            for (int i = 0; i < B_INSTR; ++i) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+        }
     };
 
-    // ---- fragment addressing ----
+    // ---- fragment offsets (lane constants; the k-step and tile index only add immediates) ----
     const int frag_row = lane & 31;
     const int frag_half = lane >> 5;
     const int wrow0 = wave_m * (BM / WM);
     const int wcol0 = wave_n * (BN / WN);
+    // A tile i, k-step s: row r_i = wrow0 + 32 i + frag_row, chunk 2s + half, swizzled by
+    // f(r_i) = f(r_0) ^ 4 (i & 1).  Offset = r_0*128 + 4096 i + 16 ((2s + half) ^ f(r_0) ^ 4(i&1)).
+    const int r0 = wrow0 + frag_row;
+    const int f0 = (r0 ^ (r0 >> 3)) & 7;
+    int a_fo[2][4];
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int st = 0; st < 4; ++st) a_fo[p][st] = r0 * kStageKBytes + 16 * ((2 * st + frag_half) ^ f0 ^ (4 * p));
     // B transpose reads: group = lane/16, g = lane%16.
+    // bf16: rows 4*h + g/4 (+8 for the upper K half), byte columns 8*(g%4) (+32 for odd groups)
+    // int8: rows 8*h + g/2 (+16 for the upper K half), byte columns 8*(g%2) (+16 for odd groups)
+    // The row's swizzle depends only on g (k mod 4 or 8), so tile j, read h, k-step s
+    // is b_fo[j] + (s*KSTEP + h*TR_ROWS) * B_PITCH.
     const int grp = lane >> 4, g16 = lane & 15;
-    // bf16: rows 4*h + g/4 (+8 for the upper K half), columns 4*(g%4) (+16 for odd groups)
-    // int8: rows 8*h + g/2 (+16 for the upper K half), columns 8*(g%2) (+16 for odd groups)
     constexpr int TR_ROWS = DT == DT_BF16 ? 4 : 8;        // rows per transpose read
+    constexpr int KSTEP = 32 / E;                         // K elements per MFMA
     const int tr_row = DT == DT_BF16 ? (g16 >> 2) : (g16 >> 1);
-    const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (grp & 1) * 32 * E / 2;
-    const int tr_khalf = (grp >> 1) * (DT == DT_BF16 ? 8 : 16);
+    const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (grp & 1) * 16 * E;
+    const int tr_khalf = (grp >> 1) * (KSTEP / 2);
+    const int bz = bswz<DT>(tr_row);
+    int b_fo[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int colb = (wcol0 + j * 32) * E + tr_colb;
+        b_fo[j] = (tr_khalf + tr_row) * B_PITCH + (((colb >> 4) ^ bz) << 4) + (colb & 15);
+    }
 
     u32x4_t fa[2][TM], fb[2][TN];
-    auto load_frags = [&](auto buf_c, int s, int slot) {
+    auto load_frags = [&](auto buf_c, auto s_c, auto slot_c) {
         constexpr int BUF = decltype(buf_c)::value;
+        constexpr int S = decltype(s_c)::value;
+        constexpr int SLOT = decltype(slot_c)::value;
         const uint8_t *const as = BUF ? a_lds1 : a_lds0;
         const uint8_t *const bs = BUF ? b_lds1 : b_lds0;
-        const int chunk = 2 * s + frag_half;
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            const int row = wrow0 + i * 32 + frag_row;
-            fa[slot][i] = *reinterpret_cast<const u32x4_t *>(as + row * kStageKBytes + swz(chunk, row) * 16);
-        }
+        for (int i = 0; i < TM; ++i)
+            fa[SLOT][i] = *reinterpret_cast<const u32x4_t *>(as + a_fo[i & 1][S] + 4096 * i);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const int colb = (wcol0 + j * 32) * E + tr_colb;          // byte column of this lane's piece
-            u32x2_t part[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int k = s * (32 / E) + tr_khalf + h * TR_ROWS + tr_row;
-                const int phys = (colb >> 4) ^ bswz<DT>(k);
-                part[h] = lds_read_tr<DT>(bs + k * B_PITCH + phys * 16 + (colb & 15));
-            }
-            fb[slot][j] = u32x4_t{part[0][0], part[0][1], part[1][0], part[1][1]};
+            const u32x2_t lo = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP) * B_PITCH);
+            const u32x2_t hi = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP + TR_ROWS) * B_PITCH);
+            fb[SLOT][j] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
         }
     };
 
@@ -867,48 +854,60 @@ void gemm_lds_kernel(KernelArgs args) {
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = acc_vec{};
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[1][i] = u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[1][j] = u32x4_t{0u, 0u, 0u, 0u};
 
-    auto compute = [&](auto buf_c) {
+    auto mfma_slot = [&](auto slot_c) {
+        constexpr int SLOT = decltype(slot_c)::value;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            if (s < 3) load_frags(buf_c, s + 1, (s + 1) & 1);
+        for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(fa[s & 1][i], fb[s & 1][j], acc[i][j]);
-        }
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(fa[SLOT][i], fb[SLOT][j], acc[i][j]);
     };
 
-    // Pipeline: stage kt+1 streams into the other LDS buffer while stage kt is
-    // consumed; each wave waits for its own loads, then the barrier publishes
-    // them to the workgroup and retires the buffer just read.  Unrolled by two
-    // so that every LDS access names its buffer statically.
-    constexpr std::integral_constant<int, 0> B0{};
-    constexpr std::integral_constant<int, 1> B1{};
-    if (nk > 0) {
-        load_stage(0, B0);
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+
+    // One stage (buffer BUF holds stage kt, visible).  On entry slot 1 holds the
+    // fragments of the previous stage's last k-step, whose MFMAs run here, under
+    // the latency of this stage's first LDS reads; on exit slot 1 holds this
+    // stage's last k-step and every wave has finished reading buffer BUF.
+    auto stage = [&](int kt, auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        using OTHER = std::integral_constant<int, 1 - BUF>;
+        load_stage(kt + 1, OTHER{});
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(buf_c, I0{}, I0{});
+        mfma_slot(I1{});
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(buf_c, I1{}, I1{});
+        mfma_slot(I0{});
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(buf_c, I2{}, I0{});
+        mfma_slot(I1{});
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(buf_c, I3{}, I1{});
+        mfma_slot(I0{});
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        load_frags(B0, 0, 0);
+    };
+
+    if (nk > 0) {
+        load_stage(0, I0{});
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
     }
-    // The scheduling fences keep each stage's loads at its start: left free, the
-    // scheduler sinks them to just before the wait that ends the stage.
     int kt = 0;
     for (; kt + 1 < nk; kt += 2) {
-        load_stage(kt + 1, B1);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(B0);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        load_frags(B1, 0, 0);
-        load_stage(kt + 2, B0);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(B1);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        load_frags(B0, 0, 0);
+        stage(kt, I0{});
+        stage(kt + 1, I1{});
     }
-    if (kt < nk) compute(B0);
+    if (kt < nk) stage(kt, I0{});
+    mfma_slot(I1{});
 
     out_t *out;
     int64_t ldo;
@@ -983,6 +982,9 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
         case 7: return launch_tile<DT, 64, 256, 1, 4, true, 2>(a, grid, s);
         case 8: return launch_direct<DT, 256, 256, 2, 2, 1>(a, grid, s);
         case 9: return launch_direct<DT, 128, 256, 2, 2, 1>(a, grid, s);
+        case 10: return launch_direct<DT, 256, 256, 2, 4, 2>(a, grid, s);
+        case 11: return launch_direct<DT, 256, 256, 4, 2, 2>(a, grid, s);
+        case 12: return launch_direct<DT, 128, 256, 2, 4, 2>(a, grid, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -72,7 +72,8 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip) {
     const int64_t slots = int64_t(chip.cus) * c.occupancy;
     const int64_t rounds = ceil_div(pl.grid, slots);
     const double wg_ops = 2.0 * c.bm * c.bn * double(pl.k_chunk);
-    const double wg_s = wg_ops / (cu_rate * c.eff / c.occupancy);
+    const double eff = p.dtype == DT_I8 ? c.eff_i8 : c.eff_bf16;
+    const double wg_s = wg_ops / (cu_rate * eff / c.occupancy);
     pl.t_comp_us = double(rounds) * wg_s * 1e6;
 
     // Memory: compulsory traffic at HBM speed; tile re-reads (Eqs. 6-7 analog)

@@ -30,9 +30,9 @@ struct Chip {
     double  clock_hz = 2.4e9;
     double  i8_ops_per_clk_cu = 8192.0;   // dense int8 MFMA
     double  bf16_ops_per_clk_cu = 4096.0; // dense bf16 MFMA
-    double  hbm_bytes_per_s = 8.0e12;
+    double  hbm_bytes_per_s = 4.0e12;     // sustained cold-HBM streaming rate the kernels reach
     double  reread_bytes_per_s = 16.0e12; // A/B tile re-reads mostly served by L2/MALL
-    double  launch_us = 2.0;              // per kernel launch on the stream
+    double  launch_us = 5.0;              // per kernel launch on the stream
 };
 
 int32_t elem_bytes(int32_t dtype);
