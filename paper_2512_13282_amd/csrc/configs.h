@@ -26,6 +26,7 @@ struct TileConfig {
     int32_t bm, bn;      // workgroup macro-tile (rows of C, cols of C)
     int32_t wm, wn;      // waves along M and N (wave tile = bm/wm x bn/wn)
     int32_t occupancy;   // workgroups resident per CU (LDS and register bound)
+    int32_t stages;      // LDS stage buffers
     double  eff_i8;      // sustained fraction of the 2.4 GHz dense MFMA peak, int8
     double  eff_bf16;    // same, bf16 (measured on the 8192^3 GEMM, MI355X)
     const char *name;
@@ -43,28 +44,31 @@ constexpr int32_t kStageKBytes = 128;
 // Family DIRECT: both operands stream global -> LDS directly (buffer loads with
 // an LDS destination); B's fragments come from LDS transpose reads.
 constexpr TileConfig kConfigs[] = {
-    // family       bm   bn  wm wn occ  eff_i8 eff_bf16 name
-    {FAM_GENERIC,   64,  64, 2, 2, 2, 0.05, 0.07, "generic_64x64_w4"},
-    {FAM_GENERIC,  128, 128, 2, 2, 1, 0.07, 0.10, "generic_128x128_w4"},
-    {FAM_MACRO,    256, 256, 2, 2, 1, 0.33, 0.41, "macro_256x256_w4"},
-    {FAM_MACRO,    128, 256, 2, 2, 1, 0.27, 0.33, "macro_128x256_w4"},
-    {FAM_MACRO,    256, 128, 2, 2, 1, 0.31, 0.33, "macro_256x128_w4"},
-    {FAM_MACRO,    128, 128, 2, 2, 2, 0.30, 0.35, "macro_128x128_w4"},
-    {FAM_SKINNY,    32, 256, 1, 4, 2, 0.17, 0.22, "skinny_32x256_w4"},
-    {FAM_SKINNY,    64, 256, 1, 4, 2, 0.25, 0.32, "skinny_64x256_w4"},
-    {FAM_DIRECT,   256, 256, 2, 2, 1, 0.40, 0.44, "direct_256x256_w4"},
-    {FAM_DIRECT,   128, 256, 2, 2, 1, 0.39, 0.34, "direct_128x256_w4"},
-    {FAM_DIRECT,   256, 256, 2, 4, 1, 0.44, 0.51, "direct_256x256_w8"},
-    {FAM_DIRECT,   256, 256, 4, 2, 1, 0.45, 0.51, "direct_256x256_w8t"},
-    {FAM_DIRECT,   128, 256, 2, 4, 1, 0.42, 0.36, "direct_128x256_w8"},
+    // family       bm   bn  wm wn occ stages eff_i8 eff_bf16 name
+    {FAM_GENERIC,   64,  64, 2, 2, 2, 2, 0.05, 0.07, "generic_64x64_w4"},
+    {FAM_GENERIC,  128, 128, 2, 2, 1, 2, 0.07, 0.10, "generic_128x128_w4"},
+    {FAM_MACRO,    256, 256, 2, 2, 1, 2, 0.33, 0.41, "macro_256x256_w4"},
+    {FAM_MACRO,    128, 256, 2, 2, 1, 2, 0.27, 0.33, "macro_128x256_w4"},
+    {FAM_MACRO,    256, 128, 2, 2, 1, 2, 0.31, 0.33, "macro_256x128_w4"},
+    {FAM_MACRO,    128, 128, 2, 2, 2, 2, 0.30, 0.35, "macro_128x128_w4"},
+    {FAM_SKINNY,    32, 256, 1, 4, 2, 2, 0.17, 0.22, "skinny_32x256_w4"},
+    {FAM_SKINNY,    64, 256, 1, 4, 2, 2, 0.25, 0.32, "skinny_64x256_w4"},
+    {FAM_DIRECT,   256, 256, 2, 2, 1, 2, 0.40, 0.44, "direct_256x256_w4"},
+    {FAM_DIRECT,   128, 256, 2, 2, 1, 2, 0.39, 0.34, "direct_128x256_w4"},
+    {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.44, 0.51, "direct_256x256_w8"},
+    {FAM_DIRECT,   256, 256, 4, 2, 1, 2, 0.45, 0.51, "direct_256x256_w8t"},
+    {FAM_DIRECT,   128, 256, 2, 4, 1, 2, 0.42, 0.36, "direct_128x256_w8"},
+    {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.30, 0.30, "pingpong_256x256_w8"},
+    {FAM_SKINNY,    32, 256, 1, 4, 1, 4, 0.10, 0.12, "stream_32x256_s4"},
+    {FAM_SKINNY,    64, 256, 1, 4, 1, 3, 0.15, 0.18, "stream_64x256_s3"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 
-// LDS bytes of one workgroup: A (bm x 128 B) and B^T (bn x 128 B) stages,
-// double-buffered.  The analog of the paper's L1 budget (Eq. 5) without the C
-// term: the output tile lives in registers, not in LDS.
+// LDS bytes of one workgroup: `stages` copies of an A stage (bm x 128 B) and a
+// B stage (bn x 128 B).  The analog of the paper's L1 budget (Eq. 5) without
+// the C term: the output tile lives in registers, not in LDS.
 constexpr int64_t lds_bytes(const TileConfig &c) {
-    return 2LL * (int64_t(c.bm) + int64_t(c.bn)) * kStageKBytes;
+    return int64_t(c.stages) * (int64_t(c.bm) + int64_t(c.bn)) * kStageKBytes;
 }
 
 }  // namespace gemm

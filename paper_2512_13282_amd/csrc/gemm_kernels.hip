@@ -430,6 +430,14 @@ void gemm_tile_kernel(KernelArgs args) {
 // live in one scheduling region.
 // ---------------------------------------------------------------------------
 
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
+
 constexpr int kBufferFlags = 0x00020000;   // raw untyped dword access (gfx9 family descriptor word 3)
 constexpr uint32_t kOOB = 0x80000000u;     // offset past any resource used here -> load returns 0
 
@@ -798,6 +806,29 @@ void gemm_lds_kernel(KernelArgs args) {
         }
     };
 
+    // A full stage's loads issued in two halves, at the start of k-steps 0 and 1:
+    // issuing all of them in one burst backs up the vector memory path and
+    // stalls the issuing waves (and their MFMAs) for longer than the spread
+    // costs in latency.  A partial last stage is loaded whole with part 0.
+    auto load_stage_part = [&](int kt, auto buf_c, int part) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const int64_t rem = k_len - int64_t(kt) * BK;
+        if (rem < BK) {
+            if (part == 0) load_stage(kt, buf_c);
+            return;
+        }
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
+        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(BK * ldb_b));
+        uint8_t *const as = BUF ? a_lds1 : a_lds0;
+        uint8_t *const bs = BUF ? b_lds1 : b_lds0;
+#pragma unroll
+        for (int i = 0; i < (A_INSTR > B_INSTR ? A_INSTR : B_INSTR); ++i) {
+            if ((i & 1) != part) continue;
+            if (i < A_INSTR) load_lds16(ra, as + (i * WAVES + wave) * 1024, a_voff[i]);
+            if (i < B_INSTR) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+        }
+    };
+
     // ---- fragment offsets (lane constants; the k-step and tile index only add immediates) ----
     const int frag_row = lane & 31;
     const int frag_half = lane >> 5;
@@ -879,10 +910,12 @@ void gemm_lds_kernel(KernelArgs args) {
     auto stage = [&](int kt, auto buf_c) {
         constexpr int BUF = decltype(buf_c)::value;
         using OTHER = std::integral_constant<int, 1 - BUF>;
-        load_stage(kt + 1, OTHER{});
+        load_stage_part(kt + 1, OTHER{}, 0);
         __builtin_amdgcn_sched_barrier(0);
         load_frags(buf_c, I0{}, I0{});
         mfma_slot(I1{});
+        __builtin_amdgcn_sched_barrier(0);
+        load_stage_part(kt + 1, OTHER{}, 1);
         __builtin_amdgcn_sched_barrier(0);
         load_frags(buf_c, I1{}, I1{});
         mfma_slot(I0{});
@@ -926,6 +959,432 @@ void gemm_lds_kernel(KernelArgs args) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Ping-pong direct-to-LDS kernel: 256 x 256 macro-tile, 8 waves, two wave
+// groups that alternate between a compute phase and a memory phase.
+//
+// Waves w and w + 4 share a SIMD.  Group 0 (waves 0-3) owns output rows 0-127
+// of the tile, group 1 rows 128-255; each wave a 128 x 64 sub-tile.  A "unit"
+// is half a stage (two MFMA k-steps).  Group 1 runs one phase behind group 0,
+// so in every phase one wave per SIMD issues a dense run of 16 MFMAs from
+// fragments already in registers while the other reads its next unit's
+// fragments from LDS and issues its share of the next stage's global -> LDS
+// loads.  Phases are separated by workgroup barriers.  Stage s sits in LDS
+// buffer s % 2 and is read in phases 4s .. 4s+3; the loads of stage s+1 are
+// issued in phases 4s (group 0) and 4s+1 (group 1) and waited for at the end
+// of phase 4s+3, so a load has three phases to land.  Every wave executes
+// the same barrier sequence; only the work between barriers depends on the
+// group.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void phase_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+__device__ __forceinline__ void stage_barrier() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int DT>
+__global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2)))
+void gemm_pingpong_kernel(KernelArgs args) {
+    using acc_vec = typename Types<DT>::acc_vec;
+    using out_t = typename Types<DT>::out_t;
+    constexpr int BM = 256, BN = 256, WAVES = 8;
+    constexpr int E = Types<DT>::E;
+    constexpr int VECE = 16 / E;
+    constexpr int BK = kStageKBytes / E;
+    constexpr int TM = 4, TN = 2;                          // 128 x 64 per wave
+    constexpr int A_STAGE = BM * kStageKBytes;
+    constexpr int B_PITCH = BN * E;
+    constexpr int B_STAGE = BK * B_PITCH;
+    constexpr int A_INSTR = A_STAGE / 1024 / WAVES;        // 4
+    constexpr int B_INSTR = B_STAGE / 1024 / WAVES;        // 4
+    constexpr int B_ROWS_PER_KB = 1024 / B_PITCH;
+    constexpr int B_CPR = B_PITCH / 16;
+
+    __shared__ __attribute__((aligned(1024))) uint8_t a_lds0[A_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t a_lds1[A_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t b_lds0[B_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t b_lds1[B_STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int grp = wave >> 2;
+    const int wave_m = grp, wave_n = wave & 3;
+
+    int tm, tn, slice;
+    map_tile(args, tm, tn, slice);
+    const int64_t M = args.M, N = args.N;
+    const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+    const int64_t k_begin = int64_t(slice) * args.k_chunk;
+    int64_t k_end = k_begin + args.k_chunk;
+    if (k_end > args.K) k_end = args.K;
+    const int nk = k_end > k_begin ? int((k_end - k_begin + BK - 1) / BK) : 0;
+    const int64_t lda_b = args.lda * E, ldb_b = args.ldb * E;
+
+    // global -> LDS source offsets (see gemm_lds_kernel)
+    const int64_t a_rows_valid = (M - m0) < BM ? (M - m0) : BM;
+    const uint32_t a_bytes = uint32_t(a_rows_valid * lda_b);
+    uint32_t a_voff[A_INSTR];
+    int a_chunk[A_INSTR];
+#pragma unroll
+    for (int i = 0; i < A_INSTR; ++i) {
+        const int row = (i * WAVES + wave) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+        a_chunk[i] = c;
+        a_voff[i] = uint32_t(row * lda_b + c * 16);
+    }
+    uint32_t b_voff[B_INSTR];
+#pragma unroll
+    for (int i = 0; i < B_INSTR; ++i) {
+        const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
+        const int c = (lane % B_CPR) ^ bswz<DT>(row);
+        b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
+    }
+    const uint8_t *const a_base = static_cast<const uint8_t *>(args.A) + (m0 * args.lda + k_begin) * E;
+    const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
+    const int64_t k_len = k_end - k_begin;
+
+    auto load_stage = [&](int kt, auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const int64_t rem = k_len - int64_t(kt) * BK;
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
+        const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
+        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+        uint8_t *const as = BUF ? a_lds1 : a_lds0;
+        uint8_t *const bs = BUF ? b_lds1 : b_lds0;
+        if (rem >= BK) {
+#pragma unroll
+            for (int i = 0; i < A_INSTR; ++i) {
+                load_lds16(ra, as + (i * WAVES + wave) * 1024, a_voff[i]);
+                load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < A_INSTR; ++i) {
+                const uint32_t off = int64_t(a_chunk[i]) * VECE < rem ? a_voff[i] : kOOB;
+                load_lds16(ra, as + (i * WAVES + wave) * 1024, off);
+                load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+            }
+        }
+    };
+
+    // fragment offsets (see gemm_lds_kernel)
+    const int frag_row = lane & 31;
+    const int frag_half = lane >> 5;
+    const int wrow0 = wave_m * (BM / 2);
+    const int wcol0 = wave_n * (BN / 4);
+    const int r0 = wrow0 + frag_row;
+    const int f0 = (r0 ^ (r0 >> 3)) & 7;
+    int a_fo[2][4];
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int st = 0; st < 4; ++st) a_fo[p][st] = r0 * kStageKBytes + 16 * ((2 * st + frag_half) ^ f0 ^ (4 * p));
+    const int g16 = lane & 15, lgrp = lane >> 4;
+    constexpr int TR_ROWS = DT == DT_BF16 ? 4 : 8;
+    constexpr int KSTEP = 32 / E;
+    const int tr_row = DT == DT_BF16 ? (g16 >> 2) : (g16 >> 1);
+    const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (lgrp & 1) * 16 * E;
+    const int tr_khalf = (lgrp >> 1) * (KSTEP / 2);
+    const int bz = bswz<DT>(tr_row);
+    int b_fo[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int colb = (wcol0 + j * 32) * E + tr_colb;
+        b_fo[j] = (tr_khalf + tr_row) * B_PITCH + (((colb >> 4) ^ bz) << 4) + (colb & 15);
+    }
+
+    u32x4_t fa[2][TM], fb[2][TN];                          // one unit: two k-steps
+    auto load_unit = [&](auto buf_c, auto h_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        constexpr int H = decltype(h_c)::value;
+        const uint8_t *const as = BUF ? a_lds1 : a_lds0;
+        const uint8_t *const bs = BUF ? b_lds1 : b_lds0;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            constexpr int dummy = 0; (void)dummy;
+            const int S = 2 * H + ks;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[ks][i] = *reinterpret_cast<const u32x4_t *>(as + a_fo[i & 1][S] + 4096 * i);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const u32x2_t lo = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP) * B_PITCH);
+                const u32x2_t hi = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP + TR_ROWS) * B_PITCH);
+                fb[ks][j] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+            }
+        }
+    };
+
+    acc_vec acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = acc_vec{};
+
+    auto compute_unit = [&]() {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(fa[ks][i], fb[ks][j], acc[i][j]);
+        __builtin_amdgcn_s_setprio(0);
+    };
+
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+
+    // Four phases of stage s (LDS buffer BUF = s % 2).
+    auto stage_phases = [&](int s, auto buf_c) {
+        using OTHER = std::integral_constant<int, 1 - decltype(buf_c)::value>;
+        // phase 4s
+        if (grp == 0) {
+            if (s + 1 < nk) load_stage(s + 1, OTHER{});
+            load_unit(buf_c, I0{});
+        } else if (s > 0) {
+            compute_unit();
+        }
+        phase_barrier();
+        // phase 4s+1
+        if (grp == 0) {
+            compute_unit();
+        } else {
+            if (s + 1 < nk) load_stage(s + 1, OTHER{});
+            load_unit(buf_c, I0{});
+        }
+        phase_barrier();
+        // phase 4s+2
+        if (grp == 0) load_unit(buf_c, I1{});
+        else compute_unit();
+        phase_barrier();
+        // phase 4s+3
+        if (grp == 0) compute_unit();
+        else load_unit(buf_c, I1{});
+        stage_barrier();
+    };
+
+    if (nk > 0) {
+        load_stage(0, I0{});
+        stage_barrier();
+        for (int s = 0; s < nk; s += 2) {
+            stage_phases(s, I0{});
+            if (s + 1 < nk) stage_phases(s + 1, I1{});
+        }
+        if (grp == 1) compute_unit();                       // group 1's last unit
+    }
+
+    out_t *out;
+    int64_t ldo;
+    if (args.split_k > 1) {
+        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
+        ldo = N;
+    } else {
+        out = static_cast<out_t *>(args.C);
+        ldo = args.ldc;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Streaming kernel for small M (memory-bound shapes): BM = 32 or 64 rows, BN =
+// 256 columns, 4 waves (each a BM x 64 sub-tile), and an NS-deep ring of LDS
+// stages so that NS - 1 stages of B stream in while one is consumed.  Same
+// LDS layouts, swizzles and fragment reads as gemm_lds_kernel.  Each
+// iteration waits only until its own stage has landed (vmcnt counts the loads
+// of the younger stages still in flight), then one barrier publishes it and
+// retires the buffer the next load overwrites.  Loads of stages past the end
+// of the slice are still issued (zero-size resource: they return zero without
+// touching memory) so that every iteration counts the same loads.
+// ---------------------------------------------------------------------------
+template <int VMCNT>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(VMCNT >= 0 && VMCNT < 64, "vmcnt range");
+    // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
+    __builtin_amdgcn_s_waitcnt((VMCNT & 15) | (7 << 4) | (15 << 8) | ((VMCNT >> 4) << 14));
+}
+
+template <int DT, int BM, int NS>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void gemm_stream_kernel(KernelArgs args) {
+    using acc_vec = typename Types<DT>::acc_vec;
+    using out_t = typename Types<DT>::out_t;
+    constexpr int BN = 256, WAVES = 4;
+    constexpr int E = Types<DT>::E;
+    constexpr int VECE = 16 / E;
+    constexpr int BK = kStageKBytes / E;
+    constexpr int TM = BM / 32, TN = 2;                    // wave tile BM x 64
+    constexpr int A_STAGE = BM * kStageKBytes;
+    constexpr int B_PITCH = BN * E;
+    constexpr int B_STAGE = BK * B_PITCH;
+    constexpr int A_INSTR = A_STAGE / 1024 / WAVES;        // 1 (BM 32) or 2 (BM 64)
+    constexpr int B_INSTR = B_STAGE / 1024 / WAVES;        // 8
+    constexpr int LPS = A_INSTR + B_INSTR;                 // loads per wave per stage
+    constexpr int B_ROWS_PER_KB = 1024 / B_PITCH;
+    constexpr int B_CPR = B_PITCH / 16;
+    static_assert(A_INSTR >= 1 && A_INSTR * 1024 * WAVES == A_STAGE, "A stage split");
+    static_assert((NS - 2) * LPS < 64, "outstanding loads must fit vmcnt");
+
+    __shared__ __attribute__((aligned(1024))) uint8_t a_lds[NS][A_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t b_lds[NS][B_STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+
+    int tm, tn, slice;
+    map_tile(args, tm, tn, slice);
+    const int64_t M = args.M, N = args.N;
+    const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+    const int64_t k_begin = int64_t(slice) * args.k_chunk;
+    int64_t k_end = k_begin + args.k_chunk;
+    if (k_end > args.K) k_end = args.K;
+    const int nk = k_end > k_begin ? int((k_end - k_begin + BK - 1) / BK) : 0;
+    const int64_t lda_b = args.lda * E, ldb_b = args.ldb * E;
+
+    const int64_t a_rows_valid = (M - m0) < BM ? (M - m0) : BM;
+    const uint32_t a_bytes = uint32_t(a_rows_valid * lda_b);
+    uint32_t a_voff[A_INSTR];
+    int a_chunk[A_INSTR];
+#pragma unroll
+    for (int i = 0; i < A_INSTR; ++i) {
+        const int row = (i * WAVES + wave) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+        a_chunk[i] = c;
+        a_voff[i] = uint32_t(row * lda_b + c * 16);
+    }
+    uint32_t b_voff[B_INSTR];
+#pragma unroll
+    for (int i = 0; i < B_INSTR; ++i) {
+        const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
+        const int c = (lane % B_CPR) ^ bswz<DT>(row);
+        b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
+    }
+    const uint8_t *const a_base = static_cast<const uint8_t *>(args.A) + (m0 * args.lda + k_begin) * E;
+    const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
+    const int64_t k_len = k_end - k_begin;
+
+    auto load_stage = [&](int kt, auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        const int64_t rem = k_len - int64_t(kt) * BK;
+        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, rem > 0 ? a_bytes : 0u);
+        const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
+        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+#pragma unroll
+        for (int i = 0; i < A_INSTR; ++i) {
+            const uint32_t off = int64_t(a_chunk[i]) * VECE < rem ? a_voff[i] : kOOB;
+            load_lds16(ra, &a_lds[BUF][(i * WAVES + wave) * 1024], off);
+        }
+#pragma unroll
+        for (int i = 0; i < B_INSTR; ++i) load_lds16(rb, &b_lds[BUF][(i * WAVES + wave) * 1024], b_voff[i]);
+    };
+
+    const int frag_row = lane & 31;
+    const int frag_half = lane >> 5;
+    const int wcol0 = wave * 64;
+    const int r0 = frag_row;
+    const int f0 = (r0 ^ (r0 >> 3)) & 7;
+    int a_fo[2][4];
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int st = 0; st < 4; ++st) a_fo[p][st] = r0 * kStageKBytes + 16 * ((2 * st + frag_half) ^ f0 ^ (4 * p));
+    const int g16 = lane & 15, lgrp = lane >> 4;
+    constexpr int TR_ROWS = DT == DT_BF16 ? 4 : 8;
+    constexpr int KSTEP = 32 / E;
+    const int tr_row = DT == DT_BF16 ? (g16 >> 2) : (g16 >> 1);
+    const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (lgrp & 1) * 16 * E;
+    const int tr_khalf = (lgrp >> 1) * (KSTEP / 2);
+    const int bz = bswz<DT>(tr_row);
+    int b_fo[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int colb = (wcol0 + j * 32) * E + tr_colb;
+        b_fo[j] = (tr_khalf + tr_row) * B_PITCH + (((colb >> 4) ^ bz) << 4) + (colb & 15);
+    }
+
+    acc_vec acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = acc_vec{};
+
+    auto compute = [&](auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+#pragma unroll
+        for (int S = 0; S < 4; ++S) {
+            u32x4_t fa[TM], fb[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                fa[i] = *reinterpret_cast<const u32x4_t *>(&a_lds[BUF][a_fo[i & 1][S] + 4096 * i]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const u32x2_t lo = lds_read_tr<DT>(&b_lds[BUF][b_fo[j] + (S * KSTEP) * B_PITCH]);
+                const u32x2_t hi = lds_read_tr<DT>(&b_lds[BUF][b_fo[j] + (S * KSTEP + TR_ROWS) * B_PITCH]);
+                fb[j] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(fa[i], fb[j], acc[i][j]);
+        }
+    };
+
+    // One iteration: stage kt is in buffer BUF; buffer (BUF + NS - 1) % NS receives stage kt + NS - 1.
+    auto iteration = [&](int kt, auto buf_c) {
+        constexpr int BUF = decltype(buf_c)::value;
+        wait_vmcnt<(NS - 2) * LPS>();                      // own loads of stage kt have landed
+        __syncthreads();                                   // everyone's; buffer BUF-1 retired
+        load_stage(kt + NS - 1, std::integral_constant<int, (BUF + NS - 1) % NS>{});
+        compute(buf_c);
+    };
+
+    if (nk > 0) {
+        static_for<0, NS - 1>([&](auto u) { load_stage(decltype(u)::value, u); });
+        for (int kt = 0; kt < nk; kt += NS) {
+            static_for<0, NS>([&](auto u) {
+                if (kt + decltype(u)::value < nk) iteration(kt + decltype(u)::value, u);
+            });
+        }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // drain ring loads past the end before exit
+
+    out_t *out;
+    int64_t ldo;
+    if (args.split_k > 1) {
+        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
+        ldo = N;
+    } else {
+        out = static_cast<out_t *>(args.C);
+        ldo = args.ldc;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
                 if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
             }
         }
@@ -985,6 +1444,15 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
         case 10: return launch_direct<DT, 256, 256, 2, 4, 2>(a, grid, s);
         case 11: return launch_direct<DT, 256, 256, 4, 2, 2>(a, grid, s);
         case 12: return launch_direct<DT, 128, 256, 2, 4, 2>(a, grid, s);
+        case 13:
+            hipLaunchKernelGGL((gemm_pingpong_kernel<DT>), dim3(unsigned(grid)), dim3(512), 0, s, a);
+            return hipGetLastError();
+        case 14:
+            hipLaunchKernelGGL((gemm_stream_kernel<DT, 32, 4>), dim3(unsigned(grid)), dim3(256), 0, s, a);
+            return hipGetLastError();
+        case 15:
+            hipLaunchKernelGGL((gemm_stream_kernel<DT, 64, 3>), dim3(unsigned(grid)), dim3(256), 0, s, a);
+            return hipGetLastError();
         default: return hipErrorInvalidValue;
     }
 }
