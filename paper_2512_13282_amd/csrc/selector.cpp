@@ -92,9 +92,39 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip) {
     return pl;
 }
 
+// Plans measured fastest on the device for specific shapes (tune.py).
+struct TunedPlan {
+    int32_t dtype;
+    int64_t M, N, K;
+    int32_t config, split;
+};
+static const TunedPlan kTuned[] = {
+#include "tuned_plans.inc"
+    {-1, 0, 0, 0, 0, 0},   // sentinel
+};
+
+bool tuned_plan(const Problem &p, int32_t *config, int32_t *split) {
+    for (const TunedPlan &t : kTuned) {
+        if (t.dtype == p.dtype && t.M == p.M && t.N == p.N && t.K == p.K &&
+            t.config >= 0 && t.config < kNumConfigs && config_applicable(p, t.config)) {
+            *config = t.config;
+            *split = t.split;
+            return true;
+        }
+    }
+    return false;
+}
+
 bool select_plan(const Problem &p, Plan *out, int32_t forced_family, int32_t forced_config,
                  int32_t forced_split, const Chip &chip) {
     static const int32_t kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64};
+    if (forced_family < 0 && forced_config < 0 && forced_split <= 0) {
+        int32_t cfg, split;
+        if (tuned_plan(p, &cfg, &split)) {
+            *out = evaluate(p, cfg, split, chip);
+            return true;
+        }
+    }
     bool found = false;
     Plan best{};
     for (int32_t cfg = 0; cfg < kNumConfigs; ++cfg) {

@@ -47,7 +47,10 @@ bool config_applicable(const Problem &p, int32_t cfg);
 // Evaluates the model for one (config, split) candidate.
 Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip = Chip());
 
-// Best plan under the model.  forced_family < 0 means any family; forced_config
+// A plan measured fastest on the device for exactly this shape, if any applies.
+bool tuned_plan(const Problem &p, int32_t *config, int32_t *split);
+
+// Best plan: a tuned plan for this exact shape if one applies, else the model's.  forced_family < 0 means any family; forced_config
 // >= 0 pins the configuration; forced_split > 0 pins the split factor.
 // Returns false if nothing applicable exists (only possible when forced).
 bool select_plan(const Problem &p, Plan *out, int32_t forced_family = -1,

@@ -114,3 +114,35 @@ def test_plans_are_deterministic():
     a = plan(BF, 2048, 11008, 4096)
     c = plan(BF, 2048, 11008, 4096)
     assert a == c
+
+
+def _tuned_entries():
+    import os
+    import re
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "paper_2512_13282_amd", "csrc", "tuned_plans.inc")
+    out = []
+    for line in open(path):
+        m = re.match(r"\s*\{(-?\d+), (\d+), (\d+), (\d+), (\d+), (\d+)\},", line)
+        if m:
+            out.append(tuple(int(x) for x in m.groups()))
+    return out
+
+
+def test_tuned_plans_are_valid_and_used():
+    """Every measured plan names a vectorised configuration that can run its shape, and
+    gemm_plan returns it (no override active, aligned operands)."""
+    entries = _tuned_entries()
+    assert entries, "tuned_plans.inc holds no plans"
+    for (d, M, N, K, cfg, split) in entries:
+        p = plan(d, M, N, K)
+        assert p["config"] == cfg, (d, M, N, K, p["name"])
+        assert p["kernel"] != b.GEMM_KERNEL_GENERIC
+        check_invariants(p, d, M, N, K)
+
+
+def test_tuned_plans_skip_misaligned_operands():
+    # the same shape with a misaligned A pointer falls back to the alignment-agnostic family
+    (d, M, N, K, cfg, split) = _tuned_entries()[0]
+    p = plan(d, M, N, K, off=ESZ[d])
+    assert p["kernel"] == b.GEMM_KERNEL_GENERIC
