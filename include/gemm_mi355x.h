@@ -20,10 +20,14 @@
  *
  * Ownership: A, B and C are caller-owned DEVICE pointers on the current HIP
  * device, valid until the work queued on `stream` has completed.  The library
- * keeps no reference after a call returns.  The only memory it allocates is a
- * split-K workspace taken with hipMallocAsync on `stream` and released with
- * hipFreeAsync on the same stream (stream-ordered, so concurrent calls on
- * different streams never share it).
+ * keeps no reference after a call returns.  The only memory it allocates is
+ * the split-K workspace (partial sums and per-tile arrival counters), one per
+ * (device, stream): taken with hipMallocAsync on `stream` at the first split-K
+ * call that needs it, grown the same way (the old buffer released with
+ * hipFreeAsync on that stream), and kept until the process ends.  Calls on one
+ * stream run in order and share it safely; calls on different streams use
+ * different workspaces.  A stream handle that is destroyed and re-created with
+ * the same value while work of the old one is still running must not be used.
  *
  * Execution: every GEMM call is asynchronous on `stream` (a hipStream_t passed
  * as void*; NULL = the null stream) and never synchronizes the device.
@@ -80,6 +84,9 @@ typedef struct gemm_plan_info {
     int32_t waves;           /* wavefronts per workgroup                       */
     int32_t mfma_m, mfma_n, mfma_k;  /* MFMA instruction shape                 */
     int32_t split_k;         /* K slices (1 = no split)                        */
+    int32_t reduce_in_kernel;/* split-K partials summed by the last slice of each
+                                tile inside the GEMM kernel (1) or by a second
+                                kernel (0); 0 when split_k == 1                */
     int64_t k_chunk;         /* K elements per slice                           */
     int64_t grid;            /* workgroups of the main kernel                  */
     int64_t lds_bytes;       /* LDS per workgroup                              */
@@ -90,6 +97,14 @@ typedef struct gemm_plan_info {
     double  model_t_mem_us;  /* modelled memory time at 8 TB/s                 */
     char    name[48];        /* human-readable kernel/config name              */
 } gemm_plan_info;
+
+/* Test and benchmark hook: force the split-K reduction for every later call of
+ * `dtype` (1 = in-kernel by the last slice of each tile, 0 = separate reduction
+ * kernel, -1 = the selector's choice).  Both sum the K slices in the same fixed
+ * order, so the result does not depend on this choice.  Not thread-safe with
+ * respect to concurrent GEMM calls.  Returns GEMM_ERR_INVALID_VALUE for an
+ * unknown dtype or mode. */
+int gemm_force_reduce(int dtype, int mode);
 
 /* int8 x int8 -> int32.  Exact whenever every true sum fits in int32, which is
  * guaranteed for K <= 131071 (|a*b| <= 2^14); beyond that results wrap modulo
@@ -123,6 +138,12 @@ int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K,
  * respect to concurrent GEMM calls.  Returns GEMM_ERR_INVALID_VALUE for an
  * unknown kernel/config or a split factor < 0. */
 int gemm_force_plan(int dtype, int kernel, int config, int split_k);
+
+/* Frees the split-K workspaces the library holds (every device and stream).
+ * Synchronizes each device that holds one first, so it must not be called while
+ * another thread is issuing GEMM calls; later split-K calls allocate afresh.
+ * Returns GEMM_OK, or GEMM_ERR_HIP if a synchronization or free failed. */
+int gemm_release_workspace(void);
 
 /* Static description of the error code. */
 const char *gemm_status_string(int status);

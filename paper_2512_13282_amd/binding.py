@@ -1,7 +1,8 @@
 """Thin ctypes binding over libgemm_mi355x.so (argument marshalling only).
 
 The functions named like the C entry points (``gemm_i8_i32``, ``gemm_bf16_f32``,
-``gemm_plan``, ``gemm_force_plan``, ``gemm_status_string``, ``gemm_version``)
+``gemm_plan``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
+``gemm_status_string``, ``gemm_version``)
 take plain integers and device addresses exactly as the C ABI does.  The two
 torch helpers (``mm_i8_i32``, ``mm_bf16_f32``) only read ``data_ptr()``,
 strides and the current HIP stream of torch tensors and call the same entry
@@ -31,8 +32,8 @@ GEMM_KERNEL_MACRO = 1
 GEMM_KERNEL_SKINNY = 2
 GEMM_KERNEL_DIRECT = 3
 
-EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_plan", "gemm_force_plan",
-            "gemm_status_string", "gemm_version")
+EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_plan", "gemm_force_plan", "gemm_force_reduce",
+            "gemm_release_workspace", "gemm_status_string", "gemm_version")
 
 
 class PlanInfo(ctypes.Structure):
@@ -41,7 +42,7 @@ class PlanInfo(ctypes.Structure):
         ("bm", ctypes.c_int32), ("bn", ctypes.c_int32), ("bk", ctypes.c_int32),
         ("waves", ctypes.c_int32),
         ("mfma_m", ctypes.c_int32), ("mfma_n", ctypes.c_int32), ("mfma_k", ctypes.c_int32),
-        ("split_k", ctypes.c_int32),
+        ("split_k", ctypes.c_int32), ("reduce_in_kernel", ctypes.c_int32),
         ("k_chunk", ctypes.c_int64), ("grid", ctypes.c_int64),
         ("lds_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
         ("model_traffic_bytes", ctypes.c_double),
@@ -78,6 +79,10 @@ def lib() -> ctypes.CDLL:
         l.gemm_plan.restype = i32
         l.gemm_force_plan.argtypes = [i32, i32, i32, i32]
         l.gemm_force_plan.restype = i32
+        l.gemm_force_reduce.argtypes = [i32, i32]
+        l.gemm_force_reduce.restype = i32
+        l.gemm_release_workspace.argtypes = []
+        l.gemm_release_workspace.restype = i32
         l.gemm_status_string.argtypes = [i32]
         l.gemm_status_string.restype = ctypes.c_char_p
         l.gemm_version.argtypes = []
@@ -108,6 +113,14 @@ def gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr=0, b_addr=0, c_addr=0) -> di
 
 def gemm_force_plan(dtype, kernel=GEMM_KERNEL_AUTO, config=-1, split_k=0) -> int:
     return lib().gemm_force_plan(dtype, kernel, config, split_k)
+
+
+def gemm_force_reduce(dtype, mode=-1) -> int:
+    return lib().gemm_force_reduce(dtype, mode)
+
+
+def gemm_release_workspace() -> int:
+    return lib().gemm_release_workspace()
 
 
 def gemm_status_string(status: int) -> str:

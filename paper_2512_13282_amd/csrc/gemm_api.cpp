@@ -23,6 +23,7 @@ struct Override {
     int32_t family = -1;   // -1 = automatic
     int32_t config = -1;
     int32_t split = 0;
+    int32_t reduce = -1;   // -1 = automatic
 };
 
 std::mutex g_mu;
@@ -88,7 +89,7 @@ int plan_for(const Problem &p, Plan *out) {
         std::lock_guard<std::mutex> lk(g_mu);
         ov = g_override[p.dtype];
     }
-    const bool forced = ov.family >= 0 || ov.config >= 0 || ov.split > 0;
+    const bool forced = ov.family >= 0 || ov.config >= 0 || ov.split > 0 || ov.reduce >= 0;
     if (!forced) {
         const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p)};
         std::lock_guard<std::mutex> lk(g_mu);
@@ -99,7 +100,8 @@ int plan_for(const Problem &p, Plan *out) {
         }
     }
     Plan pl;
-    if (!gemm::select_plan(p, &pl, ov.family, ov.config, ov.split)) return GEMM_ERR_UNSUPPORTED;
+    if (!gemm::select_plan(p, &pl, ov.family, ov.config, ov.split, gemm::Chip(), ov.reduce))
+        return GEMM_ERR_UNSUPPORTED;
     if (!forced) {
         const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p)};
         std::lock_guard<std::mutex> lk(g_mu);
@@ -135,6 +137,7 @@ int run(int32_t dtype, int64_t M, int64_t N, int64_t K, const void *A, int64_t l
     a.tiles_m = int32_t(pl.tiles_m);
     a.tiles_n = int32_t(pl.tiles_n);
     a.group_m = 4;
+    a.reduce_in_kernel = pl.reduce_in_kernel;
     if (pl.grid > 0x7fffffff || pl.tiles_m > 0x7fffffff || pl.tiles_n > 0x7fffffff)
         return GEMM_ERR_UNSUPPORTED;
     const int lr = gemm::launch_gemm(a, pl.config, pl.grid, stream);
@@ -186,6 +189,7 @@ int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t l
     out->mfma_n = 32;
     out->mfma_k = dtype == GEMM_DTYPE_I8_I32 ? 32 : 16;
     out->split_k = pl.split_k;
+    out->reduce_in_kernel = pl.split_k > 1 ? pl.reduce_in_kernel : 0;
     out->k_chunk = pl.k_chunk;
     out->grid = pl.grid;
     out->lds_bytes = gemm::lds_bytes(c);
@@ -205,13 +209,27 @@ int gemm_force_plan(int dtype, int kernel, int config, int split_k) {
     std::lock_guard<std::mutex> lk(g_mu);
     Override &o = g_override[dtype];
     if (kernel == GEMM_KERNEL_AUTO && config < 0) {
-        o = Override{-1, -1, split_k};
+        o.family = -1;
+        o.config = -1;
+        o.split = split_k;
     } else {
         o.family = kernel;
         o.config = config;
         o.split = split_k;
     }
     return GEMM_OK;
+}
+
+int gemm_force_reduce(int dtype, int mode) {
+    if (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32) return GEMM_ERR_INVALID_VALUE;
+    if (mode < -1 || mode > 1) return GEMM_ERR_INVALID_VALUE;
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_override[dtype].reduce = mode;
+    return GEMM_OK;
+}
+
+int gemm_release_workspace(void) {
+    return gemm::release_workspaces() == gemm::LAUNCH_OK ? GEMM_OK : GEMM_ERR_HIP;
 }
 
 const char *gemm_status_string(int status) {

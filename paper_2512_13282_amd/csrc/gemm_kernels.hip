@@ -35,7 +35,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <map>
+#include <mutex>
 #include <type_traits>
+#include <utility>
 
 #include "configs.h"
 #include "launch.h"
@@ -99,6 +102,129 @@ __device__ __forceinline__ void map_tile(const KernelArgs &a, int &tm, int &tn, 
     const int in_group = t % width;
     tm = first_m + in_group % gsize;
     tn = in_group / gsize;
+}
+
+// Epilogue shared by every kernel: writes the accumulators of one wave (TM x
+// TN 32x32 MFMA tiles whose top-left output element is (r0, c0)) of the
+// BM x BN output tile (tm, tn) to C.
+//
+// With split-K each K slice stores its partial tile in the workspace
+// ([split][M][N]).  Then either a separate kernel sums the planes
+// (splitk_reduce_kernel), or, with args.reduce_in_kernel, every slice takes a
+// ticket from the tile's arrival counter and the workgroup that arrives last
+// sums the slices of the tile and writes C, then resets the counter to zero
+// for the next launch on the stream.  Both sum in the fixed slice order
+// 0, 1, ..., so fp32 results are identical run to run whichever slice finishes
+// last and whichever reduction runs.
+//
+// The slices of a tile run on different XCDs, whose L2 caches are not kept
+// coherent with each other for ordinary accesses.  Instead of device-scope
+// fences (which write back and invalidate the whole L2 of the XCD), the
+// partials are stored and loaded with device-scope (sc1) accesses, which go
+// to the device coherence point: each thread waits until its partial stores
+// are complete, the workgroup synchronises, and only then takes its ticket
+// (an atomic, itself coherent device-wide); the partial loads of the last
+// workgroup depend on the ticket and are issued after it.
+template <typename T>
+__device__ __forceinline__ void store_coherent(T *p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T load_coherent(const T *p) {
+    return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int DT, int BM, int BN, int TM, int TN>
+__device__ __forceinline__ void store_tile(const KernelArgs &args,
+                                           const typename Types<DT>::acc_vec (&acc)[TM][TN],
+                                           int tm, int tn, int slice, int64_t r0, int64_t c0, int lane) {
+    using out_t = typename Types<DT>::out_t;
+    using sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;  // int32 wraps mod 2^32
+    const int frag_row = lane & 31, frag_half = lane >> 5;
+    const int64_t M = args.M, N = args.N;
+    const int64_t plane = M * N;
+    if (args.split_k == 1 || !args.reduce_in_kernel) {
+        // C itself, or this slice's partial plane for the separate reduction.
+        out_t *out = args.split_k > 1 ? static_cast<out_t *>(args.workspace) + int64_t(slice) * plane
+                                      : static_cast<out_t *>(args.C);
+        const int64_t ldo = args.split_k > 1 ? N : args.ldc;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                    if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
+                }
+            }
+        return;
+    }
+
+    sum_t *ws = static_cast<sum_t *>(args.workspace);
+    {
+        sum_t *out = ws + int64_t(slice) * plane;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                    if (row < M && col < N) store_coherent(&out[row * N + col], sum_t(acc[i][j][r]));
+                }
+            }
+    }
+    __shared__ int s_last;
+    const int tile = tm * args.tiles_n + tn;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's partial stores are complete
+    __syncthreads();                                   // ... and every thread's
+    if (threadIdx.x == 0) {
+        const unsigned ticket = __hip_atomic_fetch_add(&args.counters[tile], 1u, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+        s_last = ticket == unsigned(args.split_k - 1);
+    }
+    __syncthreads();
+    if (!s_last) return;
+
+    // Last slice of this tile: C = ((ws[0] + ws[1]) + ws[2]) + ... over the valid part of the
+    // tile, by all threads, consecutive columns per thread, with up to sixteen slices in flight.
+    out_t *C = static_cast<out_t *>(args.C);
+    const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+    const int rows = int(M - m0 < BM ? M - m0 : BM);
+    const int cols = int(N - n0 < BN ? N - n0 : BN);
+    const int split = args.split_k;
+    constexpr int V = 2;                               // columns per thread and pass
+    const int groups = (cols + V - 1) / V;
+    for (int q = int(threadIdx.x); q < rows * groups; q += int(blockDim.x)) {
+        const int rr = q / groups, cv = (q % groups) * V;
+        const int64_t base = (m0 + rr) * N + n0 + cv;
+        const int nv = cols - cv < V ? cols - cv : V;
+        sum_t s[V];
+        for (int p0 = 0; p0 < split; p0 += 16) {
+            sum_t v[16][V];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const sum_t *src = ws + int64_t(p0 + u < split ? p0 + u : 0) * plane + base;
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[u][e] = e < nv ? load_coherent(src + e) : sum_t(0);
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (p0 + u < split) {
+#pragma unroll
+                    for (int e = 0; e < V; ++e) s[e] = (p0 + u == 0) ? v[u][e] : s[e] + v[u][e];
+                }
+        }
+        out_t *dst = C + (m0 + rr) * args.ldc + n0 + cv;
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            if (e < nv) dst[e] = out_t(s[e]);
+    }
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&args.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int DT, int BM, int BN, int WM, int WN, bool VEC>
@@ -394,27 +520,7 @@ void gemm_tile_kernel(KernelArgs args) {
     }
 
     // ---------------- epilogue ----------------
-    out_t *out;
-    int64_t ldo;
-    if (args.split_k > 1) {
-        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
-        ldo = N;
-    } else {
-        out = static_cast<out_t *>(args.C);
-        ldo = args.ldc;
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
-            }
-        }
-    }
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -628,27 +734,7 @@ void gemm_vec_kernel(KernelArgs args) {
     }
     if (kt < nk) compute(0);
 
-    out_t *out;
-    int64_t ldo;
-    if (args.split_k > 1) {
-        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
-        ldo = N;
-    } else {
-        out = static_cast<out_t *>(args.C);
-        ldo = args.ldc;
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
-            }
-        }
-    }
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -942,27 +1028,7 @@ void gemm_lds_kernel(KernelArgs args) {
     if (kt < nk) stage(kt, I0{});
     mfma_slot(I1{});
 
-    out_t *out;
-    int64_t ldo;
-    if (args.split_k > 1) {
-        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
-        ldo = N;
-    } else {
-        out = static_cast<out_t *>(args.C);
-        ldo = args.ldc;
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
-            }
-        }
-    }
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1182,27 +1248,7 @@ void gemm_pingpong_kernel(KernelArgs args) {
         if (grp == 1) compute_unit();                       // group 1's last unit
     }
 
-    out_t *out;
-    int64_t ldo;
-    if (args.split_k > 1) {
-        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
-        ldo = N;
-    } else {
-        out = static_cast<out_t *>(args.C);
-        ldo = args.ldc;
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wrow0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
-            }
-        }
-    }
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1368,31 +1414,11 @@ void gemm_stream_kernel(KernelArgs args) {
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // drain ring loads past the end before exit
 
-    out_t *out;
-    int64_t ldo;
-    if (args.split_k > 1) {
-        out = static_cast<out_t *>(args.workspace) + int64_t(slice) * M * N;
-        ldo = N;
-    } else {
-        out = static_cast<out_t *>(args.C);
-        ldo = args.ldc;
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = n0 + wcol0 + j * 32 + frag_row;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
-            }
-        }
-    }
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0, n0 + wcol0, lane);
 }
 
-// Sums split-K partials [split][M][N] into C in slice order 0, 1, ... (a fixed
-// order, so fp32 results are reproducible run to run).
+// Sums split-K partials [split][M][N] into C in slice order 0, 1, ... (the
+// same fixed order as the in-kernel reduction).
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const T *__restrict__ ws, int32_t split,
                                                             int64_t M, int64_t N,
@@ -1457,36 +1483,126 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
     }
 }
 
-int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr) {
-    hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
-    KernelArgs args = a;
-    void *ws = nullptr;
-    if (args.split_k > 1) {
-        const size_t bytes = size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
-        if (hipMallocAsync(&ws, bytes, stream) != hipSuccess || ws == nullptr) {
+__global__ __launch_bounds__(256) void zero_u32_kernel(uint32_t *__restrict__ p, int64_t n) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0u;
+}
+
+// Split-K workspace, one per (device, stream): the partial planes and the
+// per-tile arrival counters.  Kept for the life of the process and grown on
+// demand, so a split-K call costs no allocation and no extra launch.  Every
+// buffer is allocated, zeroed (counters) and released in stream order on the
+// stream that uses it, so work still queued with an old buffer is unaffected
+// by its replacement.  Launches on one stream run in order and each launch
+// leaves every counter it touched at zero, which is what makes the counters
+// reusable; separate streams get separate workspaces.
+namespace {
+struct Workspace {
+    void *partials = nullptr;
+    size_t partial_bytes = 0;
+    uint32_t *counters = nullptr;
+    int64_t counter_cap = 0;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, uintptr_t>, Workspace> g_ws;
+
+size_t grow(size_t need, size_t have, size_t quantum) {
+    size_t n = need > 2 * have ? need : 2 * have;
+    return (n + quantum - 1) / quantum * quantum;
+}
+}  // namespace
+
+static int acquire_workspace(hipStream_t stream, size_t partial_bytes, int64_t tiles, void **partials,
+                             uint32_t **counters) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return LAUNCH_HIP_ERROR;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    Workspace &w = g_ws[{dev, reinterpret_cast<uintptr_t>(stream)}];
+    if (w.partial_bytes < partial_bytes) {
+        if (w.partials != nullptr && hipFreeAsync(w.partials, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
+        w.partials = nullptr;
+        const size_t bytes = grow(partial_bytes, w.partial_bytes, size_t(1) << 20);
+        w.partial_bytes = 0;
+        if (hipMallocAsync(&w.partials, bytes, stream) != hipSuccess || w.partials == nullptr) {
+            (void)hipGetLastError();
+            w.partials = nullptr;
+            return LAUNCH_NO_MEMORY;
+        }
+        w.partial_bytes = bytes;
+    }
+    if (w.counter_cap < tiles) {
+        if (w.counters != nullptr && hipFreeAsync(w.counters, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
+        w.counters = nullptr;
+        const int64_t cap = int64_t(grow(size_t(tiles), size_t(w.counter_cap), 4096));
+        w.counter_cap = 0;
+        void *p = nullptr;
+        if (hipMallocAsync(&p, size_t(cap) * 4, stream) != hipSuccess || p == nullptr) {
             (void)hipGetLastError();
             return LAUNCH_NO_MEMORY;
         }
-        args.workspace = ws;
+        int64_t blocks = (cap + 255) / 256;
+        if (blocks > 1024) blocks = 1024;
+        hipLaunchKernelGGL(zero_u32_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream,
+                           static_cast<uint32_t *>(p), cap);
+        if (hipGetLastError() != hipSuccess) {
+            (void)hipFreeAsync(p, stream);
+            return LAUNCH_HIP_ERROR;
+        }
+        w.counters = static_cast<uint32_t *>(p);
+        w.counter_cap = cap;
+    }
+    *partials = w.partials;
+    *counters = w.counters;
+    return LAUNCH_OK;
+}
+
+int release_workspaces() {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return LAUNCH_HIP_ERROR;
+    int rc = LAUNCH_OK;
+    for (auto &kv : g_ws) {
+        Workspace &w = kv.second;
+        if (w.partials == nullptr && w.counters == nullptr) continue;
+        if (hipSetDevice(kv.first.first) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+            rc = LAUNCH_HIP_ERROR;
+            continue;
+        }
+        if (w.partials != nullptr && hipFree(w.partials) != hipSuccess) rc = LAUNCH_HIP_ERROR;
+        if (w.counters != nullptr && hipFree(w.counters) != hipSuccess) rc = LAUNCH_HIP_ERROR;
+        w = Workspace{};
+    }
+    g_ws.clear();
+    if (hipSetDevice(cur) != hipSuccess) rc = LAUNCH_HIP_ERROR;
+    return rc;
+}
+
+int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr) {
+    hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+    KernelArgs args = a;
+    args.workspace = nullptr;
+    args.counters = nullptr;
+    if (args.split_k > 1) {
+        const size_t bytes = size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
+        const int64_t tiles = args.reduce_in_kernel ? int64_t(args.tiles_m) * args.tiles_n : 0;
+        const int rc = acquire_workspace(stream, bytes, tiles, &args.workspace, &args.counters);
+        if (rc != LAUNCH_OK) return rc;
     }
     hipError_t e = args.dtype == DT_I8 ? launch_config<DT_I8>(cfg, args, grid, stream)
                                        : launch_config<DT_BF16>(cfg, args, grid, stream);
-    if (e == hipSuccess && args.split_k > 1) {
+    if (e == hipSuccess && args.split_k > 1 && !args.reduce_in_kernel) {
         const int64_t total = args.M * args.N;
         int64_t blocks = (total + 255) / 256;
         if (blocks > 8192) blocks = 8192;
         if (args.dtype == DT_I8)   // unsigned adds: int32 partials wrap modulo 2^32, defined
             hipLaunchKernelGGL(splitk_reduce_kernel<uint32_t>, dim3(unsigned(blocks)), dim3(256), 0, stream,
-                               static_cast<const uint32_t *>(ws), args.split_k, args.M, args.N,
+                               static_cast<const uint32_t *>(args.workspace), args.split_k, args.M, args.N,
                                static_cast<uint32_t *>(args.C), args.ldc);
         else
             hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(unsigned(blocks)), dim3(256), 0, stream,
-                               static_cast<const float *>(ws), args.split_k, args.M, args.N,
+                               static_cast<const float *>(args.workspace), args.split_k, args.M, args.N,
                                static_cast<float *>(args.C), args.ldc);
         e = hipGetLastError();
-    }
-    if (ws) {
-        if (hipFreeAsync(ws, stream) != hipSuccess && e == hipSuccess) e = hipErrorUnknown;
     }
     return e == hipSuccess ? LAUNCH_OK : LAUNCH_HIP_ERROR;
 }

@@ -11,18 +11,24 @@ struct KernelArgs {
     const void *A;
     const void *B;
     void *C;
-    void *workspace;               // split-K partials, set by launch_gemm
+    void *workspace;               // split-K partials [split][M][N], set by launch_gemm
+    uint32_t *counters;            // split-K arrival counter per output tile (zero between launches)
     int64_t M, N, K;
     int64_t lda, ldb, ldc;         // row strides in elements
     int64_t k_chunk;               // K elements per slice
     int32_t split_k;
     int32_t tiles_m, tiles_n;      // output tiles along M and N
     int32_t group_m;               // tile-rows per group in the launch order
+    int32_t reduce_in_kernel;      // split-K: 1 = last slice of each tile sums it, 0 = separate kernel
 };
 
 enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2 };
 
 // Queues the plan's kernels on `stream` (a hipStream_t).  Never synchronizes.
 int launch_gemm(const KernelArgs &a, int32_t config, int64_t grid, void *stream);
+
+// Frees every cached split-K workspace (all devices and streams) after
+// synchronising each device that holds one.
+int release_workspaces();
 
 }  // namespace gemm

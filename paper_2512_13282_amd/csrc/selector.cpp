@@ -46,7 +46,7 @@ bool config_applicable(const Problem &p, int32_t cfg) {
     return vector_loads_ok(p);
 }
 
-Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip) {
+Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, int32_t reduce) {
     const TileConfig &c = kConfigs[cfg];
     const int64_t e = elem_bytes(p.dtype);
     const int64_t bk = stage_k_elems(p.dtype);
@@ -87,8 +87,21 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip) {
     pl.t_mem_us = ((a_bytes + b_bytes + c_bytes + ws) / chip.hbm_bytes_per_s +
                    (a_reads + b_reads - a_bytes - b_bytes) / chip.reread_bytes_per_s) * 1e6;
 
-    pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + chip.launch_us +
-                    (pl.split_k > 1 ? chip.launch_us : 0.0);
+    // Split-K reduction.  In-kernel: the last slice of each tile reads the
+    // tile's partials, sixteen slices per round trip of 256 threads x 4
+    // columns, at the end of the kernel.  Separate: one more launch streaming
+    // the partial planes.
+    double red_us = 0.0;
+    pl.reduce_in_kernel = 0;
+    if (pl.split_k > 1) {
+        const int64_t rows = std::min<int64_t>(c.bm, p.M), cols = std::min<int64_t>(c.bn, p.N);
+        const double trips = double(ceil_div(rows * ceil_div(cols, 4), 256)) * double(ceil_div(pl.split_k, 16));
+        const double in_kernel_us = trips * chip.round_trip_us;
+        const double separate_us = chip.launch_us;
+        pl.reduce_in_kernel = reduce >= 0 ? reduce : (in_kernel_us <= separate_us ? 1 : 0);
+        red_us = pl.reduce_in_kernel ? in_kernel_us : separate_us;
+    }
+    pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + chip.launch_us + red_us;
     return pl;
 }
 
@@ -97,18 +110,20 @@ struct TunedPlan {
     int32_t dtype;
     int64_t M, N, K;
     int32_t config, split;
+    int32_t reduce;      // -1: the model's choice
 };
 static const TunedPlan kTuned[] = {
 #include "tuned_plans.inc"
-    {-1, 0, 0, 0, 0, 0},   // sentinel
+    {-1, 0, 0, 0, 0, 0, -1},   // sentinel
 };
 
-bool tuned_plan(const Problem &p, int32_t *config, int32_t *split) {
+bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce) {
     for (const TunedPlan &t : kTuned) {
         if (t.dtype == p.dtype && t.M == p.M && t.N == p.N && t.K == p.K &&
             t.config >= 0 && t.config < kNumConfigs && config_applicable(p, t.config)) {
             *config = t.config;
             *split = t.split;
+            *reduce = t.reduce;
             return true;
         }
     }
@@ -116,12 +131,12 @@ bool tuned_plan(const Problem &p, int32_t *config, int32_t *split) {
 }
 
 bool select_plan(const Problem &p, Plan *out, int32_t forced_family, int32_t forced_config,
-                 int32_t forced_split, const Chip &chip) {
+                 int32_t forced_split, const Chip &chip, int32_t forced_reduce) {
     static const int32_t kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64};
-    if (forced_family < 0 && forced_config < 0 && forced_split <= 0) {
-        int32_t cfg, split;
-        if (tuned_plan(p, &cfg, &split)) {
-            *out = evaluate(p, cfg, split, chip);
+    if (forced_family < 0 && forced_config < 0 && forced_split <= 0 && forced_reduce < 0) {
+        int32_t cfg, split, reduce;
+        if (tuned_plan(p, &cfg, &split, &reduce)) {
+            *out = evaluate(p, cfg, split, chip, reduce);
             return true;
         }
     }
@@ -138,7 +153,7 @@ bool select_plan(const Problem &p, Plan *out, int32_t forced_family, int32_t for
         for (int32_t s : kSplits) {
             if (forced_split > 0 && s != 1) break;
             const int32_t split = forced_split > 0 ? forced_split : s;
-            Plan pl = evaluate(p, cfg, split, chip);
+            Plan pl = evaluate(p, cfg, split, chip, forced_reduce);
             if (forced_split <= 0 && pl.split_k != split) continue;   // duplicate of a smaller split
             if (!found || pl.t_total_us < best.t_total_us * (1.0 - 1e-9)) {
                 best = pl;

@@ -17,6 +17,8 @@ struct Problem {
 struct Plan {
     int32_t config;      // index into kConfigs
     int32_t split_k;     // >= 1
+    int32_t reduce_in_kernel;  // split-K partials summed by the last slice of each tile (1) or by a
+                               // separate kernel (0)
     int64_t k_chunk;     // K elements per slice (multiple of the stage depth)
     int64_t tiles_m, tiles_n;
     int64_t grid;
@@ -33,6 +35,7 @@ struct Chip {
     double  hbm_bytes_per_s = 4.0e12;     // sustained cold-HBM streaming rate the kernels reach
     double  reread_bytes_per_s = 16.0e12; // A/B tile re-reads mostly served by L2/MALL
     double  launch_us = 5.0;              // per kernel launch on the stream
+    double  round_trip_us = 1.5;          // one dependent global-memory round trip of a workgroup
 };
 
 int32_t elem_bytes(int32_t dtype);
@@ -44,17 +47,21 @@ bool vector_loads_ok(const Problem &p);
 // Whether config `cfg` can run problem `p` at all.
 bool config_applicable(const Problem &p, int32_t cfg);
 
-// Evaluates the model for one (config, split) candidate.
-Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip = Chip());
+// Evaluates the model for one (config, split) candidate.  reduce < 0 picks the
+// cheaper split-K reduction by the model, 0 / 1 pins it.
+Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip = Chip(),
+              int32_t reduce = -1);
 
-// A plan measured fastest on the device for exactly this shape, if any applies.
-bool tuned_plan(const Problem &p, int32_t *config, int32_t *split);
+// A plan measured fastest on the device for exactly this shape, if any applies
+// (*reduce = -1 when the measurement left the reduction to the model).
+bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce);
 
 // Best plan: a tuned plan for this exact shape if one applies, else the model's.  forced_family < 0 means any family; forced_config
 // >= 0 pins the configuration; forced_split > 0 pins the split factor.
 // Returns false if nothing applicable exists (only possible when forced).
+// forced_reduce >= 0 pins the split-K reduction (0 separate kernel, 1 in-kernel).
 bool select_plan(const Problem &p, Plan *out, int32_t forced_family = -1,
                  int32_t forced_config = -1, int32_t forced_split = 0,
-                 const Chip &chip = Chip());
+                 const Chip &chip = Chip(), int32_t forced_reduce = -1);
 
 }  // namespace gemm

@@ -81,10 +81,13 @@ def check_bf16(A: np.ndarray, B: np.ndarray, C: np.ndarray) -> None:
     assert err <= BF16_TOL, err
 
 
-def force(dtype: int, kernel: int = b.GEMM_KERNEL_AUTO, config: int = -1, split: int = 0) -> None:
+def force(dtype: int, kernel: int = b.GEMM_KERNEL_AUTO, config: int = -1, split: int = 0,
+          reduce: int = -1) -> None:
     assert b.gemm_force_plan(dtype, kernel, config, split) == b.GEMM_OK
+    assert b.gemm_force_reduce(dtype, reduce) == b.GEMM_OK
 
 
 def unforce() -> None:
-    b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
-    b.gemm_force_plan(BF, b.GEMM_KERNEL_AUTO, -1, 0)
+    for d in (I8, BF):
+        b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
+        b.gemm_force_reduce(d, -1)

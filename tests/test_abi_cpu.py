@@ -81,6 +81,14 @@ def test_force_plan_validation():
     assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0) == b.GEMM_OK
 
 
+def test_force_reduce_validation():
+    assert b.gemm_force_reduce(7, 0) == b.GEMM_ERR_INVALID_VALUE
+    assert b.gemm_force_reduce(I8, 2) == b.GEMM_ERR_INVALID_VALUE
+    assert b.gemm_force_reduce(I8, -2) == b.GEMM_ERR_INVALID_VALUE
+    for mode in (0, 1, -1):
+        assert b.gemm_force_reduce(I8, mode) == b.GEMM_OK
+
+
 def test_plan_invalid_arguments():
     with pytest.raises(b.GemmError):
         b.gemm_plan(I8, 4, 4, 4, 3, 4, 4, FAKE_A, FAKE_B, FAKE_C)

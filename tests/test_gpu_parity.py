@@ -53,14 +53,14 @@ VEC_SHAPES = [(1, 16, 16), (37, 48, 48), (64, 256, 128), (300, 272, 1040), (257,
 ODD_SHAPES = [(1, 1, 1), (3, 5, 7), (17, 13, 31), (65, 63, 129), (129, 255, 257), (70, 300, 1001)]
 
 
-@pytest.mark.parametrize("split", [1, 3])
+@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1)], ids=["s1", "s3sep", "s3fused"])
 @pytest.mark.parametrize("config", range(NUM_CONFIGS))
 @pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
-def test_every_config_matches_oracle(dtype, config, split):
-    g.force(dtype, b.GEMM_KERNEL_AUTO, config, split)
+def test_every_config_matches_oracle(dtype, config, split, reduce):
+    g.force(dtype, b.GEMM_KERNEL_AUTO, config, split, reduce)
     for i, (M, N, K) in enumerate(VEC_SHAPES):
         A, B = _inputs(dtype, M, N, K, seed=100 + i)
-        print(f"dtype={dtype} config={config} split={split} shape={(M, N, K)}", flush=True)
+        print(f"dtype={dtype} config={config} split={split} reduce={reduce} shape={(M, N, K)}", flush=True)
         _check(dtype, A, B, g.gemm_gpu(dtype, A, B))
     for i, (M, N, K) in enumerate(ODD_SHAPES):
         A, B = _inputs(dtype, M, N, K, seed=200 + i)
@@ -190,6 +190,68 @@ def test_int8_split_k_is_invariant():
     for o in outs[1:]:
         assert np.array_equal(o, outs[0])
     g.check_i8(A, B, outs[0])
+
+
+@pytest.mark.parametrize("config", [0, 3, 6, 8, 10, 12, 14, 15])
+def test_split_k_reductions_agree_bitwise(config):
+    """The in-kernel (last slice of each tile) and the separate reduction sum the K slices in
+    the same fixed order: bf16 results are bit-identical between them and across calls,
+    including split factors above the sixteen slices one reduction pass loads."""
+    M, N, K = 70, 600, 8192
+    A, B = _inputs(BF, M, N, K, seed=21)
+    for split in (2, 7, 16, 17, 40):
+        outs = []
+        for reduce in (0, 1, 1, 0):
+            g.force(BF, b.GEMM_KERNEL_AUTO, config, split, reduce)
+            print(f"config={config} split={split} reduce={reduce}", flush=True)
+            outs.append(g.gemm_gpu(BF, A, B).view(np.uint32))
+        for o in outs[1:]:
+            assert np.array_equal(o, outs[0]), (config, split)
+        g.check_bf16(A, B, outs[0].view(np.float32))
+
+
+def test_split_k_workspace_reuse_across_shapes_and_streams():
+    """The per-stream workspace and its arrival counters are reused by every split-K call:
+    growing and shrinking shapes, back-to-back calls without host synchronisation, and two
+    streams in flight at once all give oracle-exact int8 results."""
+    shapes = [(40, 512, 4096), (200, 1040, 2048), (8, 256, 8192), (300, 1536, 4096), (1, 48, 1024)]
+    cases = []
+    for i, (M, N, K) in enumerate(shapes):
+        A, B = _inputs(I8, M, N, K, seed=40 + i)
+        ref, _ = oracle.get().gemm_i8_i32(A, B)
+        cases.append((M, N, K, A, B, ref))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for reduce in (1, 0):
+        for config, split in ((3, 6), (6, 16), (14, 5), (10, 3)):
+            g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
+            print(f"workspace reuse config={config} split={split} reduce={reduce}", flush=True)
+            outs = []
+            for rep in range(2):
+                for j, (M, N, K, A, B, ref) in enumerate(cases):
+                    st = streams[(j + rep) % 2]
+                    dA, lda = g.to_dev(A)
+                    dB, ldb = g.to_dev(B)
+                    dC, ldc = g.out_buffer(M, N, I8)
+                    torch.cuda.synchronize()
+                    rc = b.gemm_i8_i32(M, N, K, dA.data_ptr(), lda, dB.data_ptr(), ldb, dC.data_ptr(), ldc,
+                                       st.cuda_stream)
+                    assert rc == b.GEMM_OK
+                    outs.append((dA, dB, dC, ldc, M, N, ref))
+            torch.cuda.synchronize()
+            for dA, dB, dC, ldc, M, N, ref in outs:
+                C = dC.cpu().numpy()[: M * ldc].reshape(M, ldc)[:, :N]
+                assert np.array_equal(C, ref), (config, split, reduce, M, N)
+
+
+def test_release_workspace_then_reuse():
+    M, N, K = 48, 512, 4096
+    A, B = _inputs(I8, M, N, K, seed=50)
+    for reduce in (1, 0):
+        g.force(I8, b.GEMM_KERNEL_AUTO, 14, 8, reduce)
+        g.check_i8(A, B, g.gemm_gpu(I8, A, B))
+        assert b.gemm_release_workspace() == b.GEMM_OK
+        assert b.gemm_release_workspace() == b.GEMM_OK      # nothing left: still fine
+        g.check_i8(A, B, g.gemm_gpu(I8, A, B))
 
 
 def test_bf16_split_k_is_reproducible():

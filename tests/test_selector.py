@@ -123,7 +123,7 @@ def _tuned_entries():
                         "paper_2512_13282_amd", "csrc", "tuned_plans.inc")
     out = []
     for line in open(path):
-        m = re.match(r"\s*\{(-?\d+), (\d+), (\d+), (\d+), (\d+), (\d+)\},", line)
+        m = re.match(r"\s*\{(-?\d+), (\d+), (\d+), (\d+), (\d+), (\d+), (-?\d+)\},", line)
         if m:
             out.append(tuple(int(x) for x in m.groups()))
     return out
@@ -134,15 +134,38 @@ def test_tuned_plans_are_valid_and_used():
     gemm_plan returns it (no override active, aligned operands)."""
     entries = _tuned_entries()
     assert entries, "tuned_plans.inc holds no plans"
-    for (d, M, N, K, cfg, split) in entries:
+    for (d, M, N, K, cfg, split, reduce) in entries:
         p = plan(d, M, N, K)
         assert p["config"] == cfg, (d, M, N, K, p["name"])
+        if reduce >= 0 and p["split_k"] > 1:
+            assert p["reduce_in_kernel"] == reduce
         assert p["kernel"] != b.GEMM_KERNEL_GENERIC
         check_invariants(p, d, M, N, K)
 
 
 def test_tuned_plans_skip_misaligned_operands():
     # the same shape with a misaligned A pointer falls back to the alignment-agnostic family
-    (d, M, N, K, cfg, split) = _tuned_entries()[0]
+    (d, M, N, K, cfg, split, reduce) = _tuned_entries()[0]
     p = plan(d, M, N, K, off=ESZ[d])
     assert p["kernel"] == b.GEMM_KERNEL_GENERIC
+
+
+def test_split_k_reduction_choice():
+    """A small per-tile reduction (one row of output) is summed in the GEMM kernel by the last
+    slice; a large one (many rows times many slices) by the separate kernel; forcing either
+    is reflected in the plan, and split_k == 1 reports neither."""
+    try:
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 14, 16) == b.GEMM_OK
+        small = plan(I8, 1, 4096, 14336)
+        assert small["split_k"] == 16 and small["reduce_in_kernel"] == 1
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 3, 32) == b.GEMM_OK
+        large = plan(I8, 128, 4096, 16384)
+        assert large["split_k"] == 32 and large["reduce_in_kernel"] == 0
+        for mode in (0, 1):
+            assert b.gemm_force_reduce(I8, mode) == b.GEMM_OK
+            assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == mode
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 3, 1) == b.GEMM_OK
+        assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == 0
+    finally:
+        b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
+        b.gemm_force_reduce(I8, -1)
