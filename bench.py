@@ -12,7 +12,9 @@ the CPU oracle timed on a bounded sample of the same workload.
 
 `--sweep` also times every workload of the sweep (one JSON row each, on
 stderr and in gpurun_out/sweep.jsonl); memory-bound shapes there rotate
-through enough copies of B to defeat the 256 MB last-level cache.
+through enough copies of B to defeat the 256 MB last-level cache.  The same
+two 8192^3 GEMMs with B stored column-major (the *_bt entry points) are timed
+too and reported in the `column_major_b` object (`--no-bt` skips them).
 """
 from __future__ import annotations
 
@@ -43,6 +45,7 @@ def parse():
     ap.add_argument("--size", type=int, default=8192)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bt", action="store_true", help="skip the column-major-B measurements")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--only", choices=["int8", "bf16"], default=None)
     ap.add_argument("--config", type=int, default=-1,
@@ -73,10 +76,13 @@ def traffic_for(dtype: str, M: int, N: int, K: int):
 
 
 class Workload:
-    def __init__(self, dtype, M, N, K, copies=1, seed=0):
+    """One GEMM with its operands resident on the GPU.  bt=True stores B column-major
+    (as Bt, N x K) and calls the *_bt entry points."""
+
+    def __init__(self, dtype, M, N, K, copies=1, seed=0, bt=False):
         import torch
         from paper_2512_13282_amd import binding, inputs
-        self.dtype, self.M, self.N, self.K = dtype, M, N, K
+        self.dtype, self.M, self.N, self.K, self.bt = dtype, M, N, K, bt
         self.b = binding
         A, B = inputs.make_inputs(dtype, M, N, K, seed=seed)
         self.A_host, self.B_host = A, B
@@ -84,23 +90,29 @@ class Workload:
         to = (lambda x: torch.from_numpy(x).to(dev)) if dtype == "int8" else \
              (lambda x: torch.from_numpy(x.view(np.int16)).to(dev))
         self.dA = to(A)
-        self.dBs = [to(B)] + [to(B).clone() for _ in range(copies - 1)]
+        Bdev = to(np.ascontiguousarray(B.T)) if bt else to(B)
+        self.dBs = [Bdev] + [Bdev.clone() for _ in range(copies - 1)]
+        self.ldb = K if bt else N
         self.dC = torch.empty((M, N), dtype=torch.int32 if dtype == "int8" else torch.float32, device=dev)
-        self.fn = binding.gemm_i8_i32 if dtype == "int8" else binding.gemm_bf16_f32
+        if bt:
+            self.fn = binding.gemm_i8_i32_bt if dtype == "int8" else binding.gemm_bf16_f32_bt
+        else:
+            self.fn = binding.gemm_i8_i32 if dtype == "int8" else binding.gemm_bf16_f32
         self.stream = torch.cuda.current_stream(dev)
         self.i = 0
 
     def launch(self):
         dB = self.dBs[self.i % len(self.dBs)]
         self.i += 1
-        rc = self.fn(self.M, self.N, self.K, self.dA.data_ptr(), self.K, dB.data_ptr(), self.N,
+        rc = self.fn(self.M, self.N, self.K, self.dA.data_ptr(), self.K, dB.data_ptr(), self.ldb,
                      self.dC.data_ptr(), self.N, self.stream.cuda_stream)
         if rc != 0:
             raise RuntimeError(self.b.gemm_status_string(rc))
 
     def plan(self):
-        return self.b.gemm_plan(0 if self.dtype == "int8" else 1, self.M, self.N, self.K, self.K, self.N,
-                                self.N, self.dA.data_ptr(), self.dBs[0].data_ptr(), self.dC.data_ptr())
+        return self.b.gemm_plan(0 if self.dtype == "int8" else 1, self.M, self.N, self.K, self.K, self.ldb,
+                                self.N, self.dA.data_ptr(), self.dBs[0].data_ptr(), self.dC.data_ptr(),
+                                trans_b=self.bt)
 
 
 def time_workload(w: Workload, steps: int, warmup: int):
@@ -285,6 +297,20 @@ def main():
               f"kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
         del w
 
+    bt_results = {}
+    if not args.no_bt:
+        for dtype in (["int8", "bf16"] if args.only is None else [args.only]):
+            w = Workload(dtype, S, S, S, bt=True)
+            ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+            r = summarize(w, ms, kavg, kmin)
+            r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
+            bt_results[dtype] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg",
+                                                   "pct_dense_peak", "plan", "split_k", "parity_sample_ok",
+                                                   "roofline")}
+            print(f"[bench] {dtype} {S}^3 column-major B: {r['value']} {r['unit']} ({r['pct_dense_peak']}% of "
+                  f"dense peak), kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
+            del w
+
     if args.copy_probe:
         # Elementwise copy of 512 MiB: reads 512 MiB, writes 512 MiB.  Profiled beside the
         # GEMM so FETCH_SIZE / WRITE_SIZE can be scaled by what they read for known traffic.
@@ -339,6 +365,9 @@ def main():
         if dtype != head_dtype:
             line[dtype] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg", "pct_dense_peak",
                                             "plan", "split_k", "parity_sample_ok", "roofline")}
+    if bt_results:
+        line["column_major_b"] = {"workload": f"the same GEMMs with B stored column-major (N x K), "
+                                              f"gemm_*_bt entry points", **bt_results}
     print(json.dumps(line), flush=True)
 
 

@@ -17,6 +17,10 @@
  * the M x N window (row padding beyond N) are never touched.
  *
  * Layout: A, B and C are row-major; lda, ldb, ldc are row strides in ELEMENTS.
+ * The *_bt entry points take B stored column-major instead, i.e. as its
+ * transpose Bt (N x K, row-major, row stride ldbt >= K), the layout of a
+ * PyTorch Linear weight; the paper's preferred and fastest layout (Sec. 4.3,
+ * where B in column-major order lets the cores read K-contiguous blocks).
  *
  * Ownership: A, B and C are caller-owned DEVICE pointers on the current HIP
  * device, valid until the work queued on `stream` has completed.  The library
@@ -34,7 +38,8 @@
  *
  * Errors: every entry point returns an int status (gemm_status_t) and never
  * throws or aborts.  Argument checks run on the host BEFORE any HIP call:
- *   GEMM_ERR_INVALID_VALUE  M, N or K < 0; lda < K (M, K > 0); ldb < N (K, N > 0);
+ *   GEMM_ERR_INVALID_VALUE  M, N or K < 0; lda < K (M, K > 0); ldb < N (K, N > 0;
+ *                           ldbt < K for the *_bt calls);
  *                           ldc < N (M, N > 0); a NULL pointer whose operand is
  *                           non-empty; C overlapping A or B in memory.
  *   GEMM_ERR_UNSUPPORTED    a forced plan (gemm_force_plan) that cannot run the
@@ -123,6 +128,19 @@ int gemm_bf16_f32(int64_t M, int64_t N, int64_t K,
                   const uint16_t *B, int64_t ldb,
                   float *C, int64_t ldc, void *stream);
 
+/* C = A . Bt^T with B stored column-major: C[i*ldc + j] = sum_k A[i*lda + k] *
+ * Bt[j*ldbt + k].  Same results, ownership, errors and execution as
+ * gemm_i8_i32 / gemm_bf16_f32 (the int8 result is exact, bf16 products are
+ * exact with fp32 accumulation). */
+int gemm_i8_i32_bt(int64_t M, int64_t N, int64_t K,
+                   const int8_t *A, int64_t lda,
+                   const int8_t *Bt, int64_t ldbt,
+                   int32_t *C, int64_t ldc, void *stream);
+int gemm_bf16_f32_bt(int64_t M, int64_t N, int64_t K,
+                     const uint16_t *A, int64_t lda,
+                     const uint16_t *Bt, int64_t ldbt,
+                     float *C, int64_t ldc, void *stream);
+
 /* Pure host: the plan a GEMM call with these arguments would use (alignment
  * is taken from the three addresses, which are never dereferenced).
  * Returns GEMM_OK, GEMM_ERR_INVALID_VALUE or GEMM_ERR_UNSUPPORTED. */
@@ -130,6 +148,12 @@ int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K,
               int64_t lda, int64_t ldb, int64_t ldc,
               uintptr_t a_addr, uintptr_t b_addr, uintptr_t c_addr,
               gemm_plan_info *out);
+
+/* The same for the column-major-B calls (gemm_i8_i32_bt / gemm_bf16_f32_bt). */
+int gemm_plan_bt(int dtype, int64_t M, int64_t N, int64_t K,
+                 int64_t lda, int64_t ldbt, int64_t ldc,
+                 uintptr_t a_addr, uintptr_t bt_addr, uintptr_t c_addr,
+                 gemm_plan_info *out);
 
 /* Test and benchmark hook: force the kernel family, tile configuration
  * (-1 = selector's choice within the family) and split-K factor (0 = the

@@ -13,6 +13,11 @@ row-major layouts of Sec. 4.2.2 (Memory Tile Design):
   ascending.
 
 Every function takes numpy arrays (2-D, row stride free, unit column stride).
+
+The ``*_bt`` forms take B stored column-major, i.e. as its transpose Bt (N x K),
+the layout the paper prefers for B (Sec. 4.3).  They form B = Bt^T with a plain
+transposing copy and call the row-major routine: the same products summed in
+the same k order.
 """
 from __future__ import annotations
 
@@ -121,6 +126,27 @@ class Oracle:
         if rc != 0:
             raise RuntimeError(f"oracle_gemm_bf16_f64 failed ({rc})")
         return C
+
+    # -- column-major B ------------------------------------------------------
+    @staticmethod
+    def _from_bt(Bt: np.ndarray) -> np.ndarray:
+        """B (K x N, row-major) from Bt (N x K): B[k][j] = Bt[j][k]."""
+        assert Bt.ndim == 2
+        B = np.empty((Bt.shape[1], Bt.shape[0]), dtype=Bt.dtype)   # fresh row-major buffer
+        B[...] = Bt.T
+        return B
+
+    def gemm_i8_i32_bt(self, A: np.ndarray, Bt: np.ndarray, nthreads: int | None = None):
+        """C = A @ Bt^T (int8, Bt is N x K).  Returns (C int32 M x N, overflow_count)."""
+        return self.gemm_i8_i32(A, self._from_bt(Bt), nthreads)
+
+    def gemm_bf16_f64_bt(self, A: np.ndarray, Bt: np.ndarray, nthreads: int | None = None) -> np.ndarray:
+        """C = A @ Bt^T (bf16 bits, Bt is N x K).  Returns fp64 C."""
+        return self.gemm_bf16_f64(A, self._from_bt(Bt), nthreads)
+
+    def freivalds_i8_i32_bt(self, A: np.ndarray, Bt: np.ndarray, C: np.ndarray,
+                            trials: int = 2, seed: int = 1234) -> int:
+        return self.freivalds_i8_i32(A, self._from_bt(Bt), C, trials, seed)
 
     def bf16_to_double(self, bits: int) -> float:
         return float(self.lib.oracle_bf16_to_double(int(bits)))

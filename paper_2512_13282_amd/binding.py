@@ -1,7 +1,8 @@
 """Thin ctypes binding over libgemm_mi355x.so (argument marshalling only).
 
 The functions named like the C entry points (``gemm_i8_i32``, ``gemm_bf16_f32``,
-``gemm_plan``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
+their column-major-B forms ``gemm_i8_i32_bt`` and ``gemm_bf16_f32_bt``, ``gemm_plan``,
+``gemm_plan_bt``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
 ``gemm_status_string``, ``gemm_version``)
 take plain integers and device addresses exactly as the C ABI does.  The two
 torch helpers (``mm_i8_i32``, ``mm_bf16_f32``) only read ``data_ptr()``,
@@ -32,8 +33,9 @@ GEMM_KERNEL_MACRO = 1
 GEMM_KERNEL_SKINNY = 2
 GEMM_KERNEL_DIRECT = 3
 
-EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_plan", "gemm_force_plan", "gemm_force_reduce",
-            "gemm_release_workspace", "gemm_status_string", "gemm_version")
+EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt", "gemm_plan",
+            "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",
+            "gemm_status_string", "gemm_version")
 
 
 class PlanInfo(ctypes.Structure):
@@ -74,9 +76,16 @@ def lib() -> ctypes.CDLL:
         l.gemm_i8_i32.restype = i32
         l.gemm_bf16_f32.argtypes = gemm_args
         l.gemm_bf16_f32.restype = i32
-        l.gemm_plan.argtypes = [i32, i64, i64, i64, i64, i64, i64, ctypes.c_size_t,
-                                ctypes.c_size_t, ctypes.c_size_t, ctypes.POINTER(PlanInfo)]
+        l.gemm_i8_i32_bt.argtypes = gemm_args
+        l.gemm_i8_i32_bt.restype = i32
+        l.gemm_bf16_f32_bt.argtypes = gemm_args
+        l.gemm_bf16_f32_bt.restype = i32
+        plan_args = [i32, i64, i64, i64, i64, i64, i64, ctypes.c_size_t, ctypes.c_size_t,
+                     ctypes.c_size_t, ctypes.POINTER(PlanInfo)]
+        l.gemm_plan.argtypes = plan_args
         l.gemm_plan.restype = i32
+        l.gemm_plan_bt.argtypes = plan_args
+        l.gemm_plan_bt.restype = i32
         l.gemm_force_plan.argtypes = [i32, i32, i32, i32]
         l.gemm_force_plan.restype = i32
         l.gemm_force_reduce.argtypes = [i32, i32]
@@ -100,10 +109,20 @@ def gemm_bf16_f32(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
     return lib().gemm_bf16_f32(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, stream or None)
 
 
-def gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr=0, b_addr=0, c_addr=0) -> dict:
-    """The selector's plan as a dict; raises GemmError on a bad argument."""
+def gemm_i8_i32_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, stream=0) -> int:
+    return lib().gemm_i8_i32_bt(M, N, K, A or None, lda, Bt or None, ldbt, C or None, ldc, stream or None)
+
+
+def gemm_bf16_f32_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, stream=0) -> int:
+    return lib().gemm_bf16_f32_bt(M, N, K, A or None, lda, Bt or None, ldbt, C or None, ldc, stream or None)
+
+
+def gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr=0, b_addr=0, c_addr=0, trans_b=False) -> dict:
+    """The selector's plan as a dict (gemm_plan, or gemm_plan_bt with trans_b=True, where
+    ldb is the row stride of the N x K matrix); raises GemmError on a bad argument."""
     info = PlanInfo()
-    rc = lib().gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr, ctypes.byref(info))
+    fn = lib().gemm_plan_bt if trans_b else lib().gemm_plan
+    rc = fn(dtype, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr, ctypes.byref(info))
     if rc != GEMM_OK:
         raise GemmError(rc)
     d = {f: getattr(info, f) for f, _ in PlanInfo._fields_}
@@ -137,7 +156,9 @@ def _check(rc: int) -> None:
         raise GemmError(rc)
 
 
-def _mm(fn, A, B, out, in_dtype, out_dtype):
+def _mm(fns, A, B, out, in_dtype, out_dtype):
+    """B may be row-major (stride(1) == 1) or column-major (stride(0) == 1, e.g. W.t() of
+    a contiguous N x K weight W), which selects the *_bt entry point."""
     import torch
     if A.dtype != in_dtype or B.dtype != in_dtype:
         raise TypeError(f"expected {in_dtype} operands")
@@ -145,10 +166,13 @@ def _mm(fn, A, B, out, in_dtype, out_dtype):
         raise ValueError("expected A (M x K) and B (K x N)")
     if not (A.is_cuda and B.is_cuda) or A.device != B.device:
         raise ValueError("operands must be on the same GPU")
-    if A.stride(1) != 1 or B.stride(1) != 1:
-        raise ValueError("operands must be row-major with unit column stride")
     M, K = A.shape
     N = B.shape[1]
+    if A.stride(1) != 1:
+        raise ValueError("A must be row-major with unit column stride")
+    trans_b = B.stride(1) != 1 and B.stride(0) == 1 and N > 1
+    if not trans_b and B.stride(1) != 1 and K > 1 and N > 1:
+        raise ValueError("B must be row-major or column-major")
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=A.device)
     elif out.dtype != out_dtype or tuple(out.shape) != (M, N) or out.stride(1) != 1 or out.device != A.device:
@@ -156,19 +180,23 @@ def _mm(fn, A, B, out, in_dtype, out_dtype):
     stream = torch.cuda.current_stream(A.device).cuda_stream
     # A single-row matrix has no meaningful row stride; any value >= cols is valid.
     lda = A.stride(0) if M > 1 else max(K, 1)
-    ldb = B.stride(0) if K > 1 else max(N, 1)
+    if trans_b:
+        ldb = B.stride(1) if N > 1 else max(K, 1)
+    else:
+        ldb = B.stride(0) if K > 1 else max(N, 1)
     ldc = out.stride(0) if M > 1 else max(N, 1)
+    fn = fns[1] if trans_b else fns[0]
     _check(fn(M, N, K, A.data_ptr(), lda, B.data_ptr(), ldb, out.data_ptr(), ldc, stream))
     return out
 
 
 def mm_i8_i32(A, B, out=None):
-    """C = A @ B for int8 torch tensors on the GPU; int32 result."""
+    """C = A @ B for int8 torch tensors on the GPU; int32 result.  B row- or column-major."""
     import torch
-    return _mm(gemm_i8_i32, A, B, out, torch.int8, torch.int32)
+    return _mm((gemm_i8_i32, gemm_i8_i32_bt), A, B, out, torch.int8, torch.int32)
 
 
 def mm_bf16_f32(A, B, out=None):
-    """C = A @ B for bfloat16 torch tensors on the GPU; float32 result."""
+    """C = A @ B for bfloat16 torch tensors on the GPU; float32 result.  B row- or column-major."""
     import torch
-    return _mm(gemm_bf16_f32, A, B, out, torch.bfloat16, torch.float32)
+    return _mm((gemm_bf16_f32, gemm_bf16_f32_bt), A, B, out, torch.bfloat16, torch.float32)

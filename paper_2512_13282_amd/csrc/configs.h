@@ -1,7 +1,7 @@
 // configs.h -- the tile configurations compiled into the library.
 //
 // One table, read by the host-side selector (selector.cpp) and by the launch
-// code (gemm_launch.hip), which instantiates exactly these kernels.  Pure C++:
+// code (gemm_kernels.hip), which instantiates exactly these kernels.  Pure C++:
 // no HIP headers, so the selector builds and tests on a machine without a GPU.
 //
 // Tiling levels (paper, Sec. 4.1: instruction tile r x s x t -> per-core kernel
@@ -29,6 +29,7 @@ struct TileConfig {
     int32_t stages;      // LDS stage buffers
     double  eff_i8;      // sustained fraction of the 2.4 GHz dense MFMA peak, int8
     double  eff_bf16;    // same, bf16 (measured on the 8192^3 GEMM, MI355X)
+    int32_t col_major_b; // also compiled for B stored column-major (N x K)
     const char *name;
 };
 
@@ -42,25 +43,26 @@ constexpr int32_t kStageKBytes = 128;
 // in registers); large tiles.
 // Family SKINNY: same loaders, narrow M tile for M <= 64.
 // Family DIRECT: both operands stream global -> LDS directly (buffer loads with
-// an LDS destination); B's fragments come from LDS transpose reads.
+// an LDS destination); B's fragments come from LDS transpose reads, or, for B
+// stored column-major, from 16-byte reads like A's.
 constexpr TileConfig kConfigs[] = {
-    // family       bm   bn  wm wn occ stages eff_i8 eff_bf16 name
-    {FAM_GENERIC,   64,  64, 2, 2, 2, 2, 0.05, 0.07, "generic_64x64_w4"},
-    {FAM_GENERIC,  128, 128, 2, 2, 1, 2, 0.07, 0.10, "generic_128x128_w4"},
-    {FAM_MACRO,    256, 256, 2, 2, 1, 2, 0.33, 0.41, "macro_256x256_w4"},
-    {FAM_MACRO,    128, 256, 2, 2, 1, 2, 0.27, 0.33, "macro_128x256_w4"},
-    {FAM_MACRO,    256, 128, 2, 2, 1, 2, 0.31, 0.33, "macro_256x128_w4"},
-    {FAM_MACRO,    128, 128, 2, 2, 2, 2, 0.30, 0.35, "macro_128x128_w4"},
-    {FAM_SKINNY,    32, 256, 1, 4, 2, 2, 0.17, 0.22, "skinny_32x256_w4"},
-    {FAM_SKINNY,    64, 256, 1, 4, 2, 2, 0.25, 0.32, "skinny_64x256_w4"},
-    {FAM_DIRECT,   256, 256, 2, 2, 1, 2, 0.40, 0.44, "direct_256x256_w4"},
-    {FAM_DIRECT,   128, 256, 2, 2, 1, 2, 0.39, 0.34, "direct_128x256_w4"},
-    {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.44, 0.51, "direct_256x256_w8"},
-    {FAM_DIRECT,   256, 256, 4, 2, 1, 2, 0.45, 0.51, "direct_256x256_w8t"},
-    {FAM_DIRECT,   128, 256, 2, 4, 1, 2, 0.42, 0.36, "direct_128x256_w8"},
-    {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.30, 0.30, "pingpong_256x256_w8"},
-    {FAM_SKINNY,    32, 256, 1, 4, 1, 4, 0.10, 0.12, "stream_32x256_s4"},
-    {FAM_SKINNY,    64, 256, 1, 4, 1, 3, 0.15, 0.18, "stream_64x256_s3"},
+    // family       bm   bn  wm wn occ stages eff_i8 eff_bf16 colB name
+    {FAM_GENERIC,   64,  64, 2, 2, 2, 2, 0.05, 0.07, 1, "generic_64x64_w4"},
+    {FAM_GENERIC,  128, 128, 2, 2, 1, 2, 0.07, 0.10, 1, "generic_128x128_w4"},
+    {FAM_MACRO,    256, 256, 2, 2, 1, 2, 0.33, 0.41, 0, "macro_256x256_w4"},
+    {FAM_MACRO,    128, 256, 2, 2, 1, 2, 0.27, 0.33, 0, "macro_128x256_w4"},
+    {FAM_MACRO,    256, 128, 2, 2, 1, 2, 0.31, 0.33, 0, "macro_256x128_w4"},
+    {FAM_MACRO,    128, 128, 2, 2, 2, 2, 0.30, 0.35, 0, "macro_128x128_w4"},
+    {FAM_SKINNY,    32, 256, 1, 4, 2, 2, 0.17, 0.22, 0, "skinny_32x256_w4"},
+    {FAM_SKINNY,    64, 256, 1, 4, 2, 2, 0.25, 0.32, 0, "skinny_64x256_w4"},
+    {FAM_DIRECT,   256, 256, 2, 2, 1, 2, 0.40, 0.44, 1, "direct_256x256_w4"},
+    {FAM_DIRECT,   128, 256, 2, 2, 1, 2, 0.39, 0.34, 1, "direct_128x256_w4"},
+    {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.44, 0.51, 1, "direct_256x256_w8"},
+    {FAM_DIRECT,   256, 256, 4, 2, 1, 2, 0.45, 0.51, 1, "direct_256x256_w8t"},
+    {FAM_DIRECT,   128, 256, 2, 4, 1, 2, 0.42, 0.36, 1, "direct_128x256_w8"},
+    {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.30, 0.30, 0, "pingpong_256x256_w8"},
+    {FAM_SKINNY,    32, 256, 1, 4, 1, 4, 0.10, 0.12, 0, "stream_32x256_s4"},
+    {FAM_SKINNY,    64, 256, 1, 4, 1, 3, 0.15, 0.18, 0, "stream_64x256_s3"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

@@ -33,8 +33,9 @@ struct Key {
     int32_t dtype;
     int64_t M, N, K;
     bool vec;
+    int32_t trans_b;
     bool operator==(const Key &o) const {
-        return dtype == o.dtype && M == o.M && N == o.N && K == o.K && vec == o.vec;
+        return dtype == o.dtype && M == o.M && N == o.N && K == o.K && vec == o.vec && trans_b == o.trans_b;
     }
 };
 struct KeyHash {
@@ -42,7 +43,7 @@ struct KeyHash {
         uint64_t h = 1469598103934665603ULL;
         auto mix = [&](uint64_t v) { h = (h ^ v) * 1099511628211ULL; };
         mix(uint64_t(k.dtype)); mix(uint64_t(k.M)); mix(uint64_t(k.N)); mix(uint64_t(k.K));
-        mix(uint64_t(k.vec));
+        mix(uint64_t(k.vec)); mix(uint64_t(k.trans_b));
         return size_t(h);
     }
 };
@@ -63,8 +64,10 @@ int validate(const Problem &p, const void *A, const void *B, const void *C) {
     if (p.M < 0 || p.N < 0 || p.K < 0) return GEMM_ERR_INVALID_VALUE;
     const int64_t e = gemm::elem_bytes(p.dtype);
     const bool has_a = p.M > 0 && p.K > 0, has_b = p.K > 0 && p.N > 0, has_c = p.M > 0 && p.N > 0;
+    // B is K x N row-major (rows of N), or stored column-major as N x K (rows of K).
+    const int64_t b_rows = p.trans_b ? p.N : p.K, b_cols = p.trans_b ? p.K : p.N;
     if (has_a && (A == nullptr || p.lda < p.K)) return GEMM_ERR_INVALID_VALUE;
-    if (has_b && (B == nullptr || p.ldb < p.N)) return GEMM_ERR_INVALID_VALUE;
+    if (has_b && (B == nullptr || p.ldb < b_cols)) return GEMM_ERR_INVALID_VALUE;
     if (has_c && (C == nullptr || p.ldc < p.N)) return GEMM_ERR_INVALID_VALUE;
     // Natural alignment of the element types (a misaligned int32*/float*/bf16* is not a valid pointer).
     if (has_a && (uintptr_t(A) % uintptr_t(e)) != 0) return GEMM_ERR_INVALID_VALUE;
@@ -73,12 +76,12 @@ int validate(const Problem &p, const void *A, const void *B, const void *C) {
     // Stride products must not overflow 64-bit byte offsets.
     const int64_t lim = int64_t(1) << 55;
     if (p.M > lim || p.N > lim || p.K > lim || (has_a && p.lda > lim / (p.M > 0 ? p.M : 1)) ||
-        (has_b && p.ldb > lim / (p.K > 0 ? p.K : 1)) || (has_c && p.ldc > lim / (p.M > 0 ? p.M : 1)))
+        (has_b && p.ldb > lim / (b_rows > 0 ? b_rows : 1)) || (has_c && p.ldc > lim / (p.M > 0 ? p.M : 1)))
         return GEMM_ERR_INVALID_VALUE;
     const uint64_t clen = span_bytes(p.M, p.N, p.ldc, 4);
     if (has_c && has_a && overlaps(uintptr_t(C), clen, uintptr_t(A), span_bytes(p.M, p.K, p.lda, e)))
         return GEMM_ERR_INVALID_VALUE;
-    if (has_c && has_b && overlaps(uintptr_t(C), clen, uintptr_t(B), span_bytes(p.K, p.N, p.ldb, e)))
+    if (has_c && has_b && overlaps(uintptr_t(C), clen, uintptr_t(B), span_bytes(b_rows, b_cols, p.ldb, e)))
         return GEMM_ERR_INVALID_VALUE;
     return GEMM_OK;
 }
@@ -91,7 +94,7 @@ int plan_for(const Problem &p, Plan *out) {
     }
     const bool forced = ov.family >= 0 || ov.config >= 0 || ov.split > 0 || ov.reduce >= 0;
     if (!forced) {
-        const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p)};
+        const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p), p.trans_b};
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_cache.find(key);
         if (it != g_cache.end()) {
@@ -103,7 +106,7 @@ int plan_for(const Problem &p, Plan *out) {
     if (!gemm::select_plan(p, &pl, ov.family, ov.config, ov.split, gemm::Chip(), ov.reduce))
         return GEMM_ERR_UNSUPPORTED;
     if (!forced) {
-        const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p)};
+        const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p), p.trans_b};
         std::lock_guard<std::mutex> lk(g_mu);
         if (g_cache.size() > 4096) g_cache.clear();
         g_cache.emplace(key, pl);
@@ -112,9 +115,9 @@ int plan_for(const Problem &p, Plan *out) {
     return GEMM_OK;
 }
 
-int run(int32_t dtype, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
-        int64_t ldb, void *C, int64_t ldc, void *stream) {
-    Problem p{dtype, M, N, K, lda, ldb, ldc, uintptr_t(A), uintptr_t(B), uintptr_t(C)};
+int run(int32_t dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+        const void *B, int64_t ldb, void *C, int64_t ldc, void *stream) {
+    Problem p{dtype, M, N, K, lda, ldb, ldc, uintptr_t(A), uintptr_t(B), uintptr_t(C), trans_b};
     int rc = validate(p, A, B, C);
     if (rc != GEMM_OK) return rc;
     if (M == 0 || N == 0) return GEMM_OK;
@@ -138,6 +141,7 @@ int run(int32_t dtype, int64_t M, int64_t N, int64_t K, const void *A, int64_t l
     a.tiles_n = int32_t(pl.tiles_n);
     a.group_m = 4;
     a.reduce_in_kernel = pl.reduce_in_kernel;
+    a.b_trans = trans_b;
     if (pl.grid > 0x7fffffff || pl.tiles_m > 0x7fffffff || pl.tiles_n > 0x7fffffff)
         return GEMM_ERR_UNSUPPORTED;
     const int lr = gemm::launch_gemm(a, pl.config, pl.grid, stream);
@@ -152,19 +156,29 @@ extern "C" {
 
 int gemm_i8_i32(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *B,
                 int64_t ldb, int32_t *C, int64_t ldc, void *stream) {
-    return run(gemm::DT_I8, M, N, K, A, lda, B, ldb, C, ldc, stream);
+    return run(gemm::DT_I8, 0, M, N, K, A, lda, B, ldb, C, ldc, stream);
 }
 
 int gemm_bf16_f32(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *B,
                   int64_t ldb, float *C, int64_t ldc, void *stream) {
-    return run(gemm::DT_BF16, M, N, K, A, lda, B, ldb, C, ldc, stream);
+    return run(gemm::DT_BF16, 0, M, N, K, A, lda, B, ldb, C, ldc, stream);
 }
 
-int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
-              uintptr_t a_addr, uintptr_t b_addr, uintptr_t c_addr, gemm_plan_info *out) {
+int gemm_i8_i32_bt(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *Bt,
+                   int64_t ldbt, int32_t *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_I8, 1, M, N, K, A, lda, Bt, ldbt, C, ldc, stream);
+}
+
+int gemm_bf16_f32_bt(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *Bt,
+                     int64_t ldbt, float *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_BF16, 1, M, N, K, A, lda, Bt, ldbt, C, ldc, stream);
+}
+
+static int plan_impl(int dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb,
+                     int64_t ldc, uintptr_t a_addr, uintptr_t b_addr, uintptr_t c_addr, gemm_plan_info *out) {
     if (out == nullptr || (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32))
         return GEMM_ERR_INVALID_VALUE;
-    Problem p{dtype, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr};
+    Problem p{dtype, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr, trans_b};
     int rc = validate(p, reinterpret_cast<const void *>(a_addr), reinterpret_cast<const void *>(b_addr),
                       reinterpret_cast<const void *>(c_addr));
     if (rc != GEMM_OK) return rc;
@@ -199,6 +213,16 @@ int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t l
     out->model_t_mem_us = pl.t_mem_us;
     strncpy(out->name, c.name, sizeof(out->name) - 1);
     return GEMM_OK;
+}
+
+int gemm_plan(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
+              uintptr_t a_addr, uintptr_t b_addr, uintptr_t c_addr, gemm_plan_info *out) {
+    return plan_impl(dtype, 0, M, N, K, lda, ldb, ldc, a_addr, b_addr, c_addr, out);
+}
+
+int gemm_plan_bt(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldbt, int64_t ldc,
+                 uintptr_t a_addr, uintptr_t bt_addr, uintptr_t c_addr, gemm_plan_info *out) {
+    return plan_impl(dtype, 1, M, N, K, lda, ldbt, ldc, a_addr, bt_addr, c_addr, out);
 }
 
 int gemm_force_plan(int dtype, int kernel, int config, int split_k) {

@@ -314,10 +314,11 @@ __device__ __forceinline__ void i8_transpose(const u32x2_t (&rows)[N], int base,
         }
 }
 
-template <int DT, int BM, int BN, int WM, int WN, bool VEC, int WAVES_PER_EU>
+template <int DT, int BM, int BN, int WM, int WN, bool VEC, int WAVES_PER_EU, bool BT = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
                           amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_tile_kernel(KernelArgs args) {
+    static_assert(!(VEC && BT), "the vector B loader reads row-major B only");
     using T = TileKernel<DT, BM, BN, WM, WN, VEC>;
     using acc_vec = typename Types<DT>::acc_vec;
     using out_t = typename Types<DT>::out_t;
@@ -405,16 +406,19 @@ void gemm_tile_kernel(KernelArgs args) {
         } else {
 #pragma unroll
             for (int i = 0; i < T::B_CHUNKS; ++i) {
+                // Row-major B: neighbouring threads take neighbouring columns.  Column-major
+                // B (stored N x K): neighbouring threads take neighbouring K chunks of a column.
                 const int q = i * T::THREADS + tid;
-                const int n = q % BN, c = q / BN;
+                const int n = BT ? q >> 3 : q % BN, c = BT ? q & 7 : q / BN;
                 const int64_t gn = n0 + n, gk = k0 + int64_t(c) * VECE;
                 unsigned w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
                 for (int e = 0; e < VECE; ++e) {
                     unsigned x = 0;
                     if (gn < N && gk + e < k_end) {
-                        if (E == 1) x = B[(gk + e) * ldb + gn];
-                        else x = reinterpret_cast<const uint16_t *>(B)[(gk + e) * ldb + gn];
+                        const int64_t idx = BT ? gn * ldb + gk + e : (gk + e) * ldb + gn;
+                        if (E == 1) x = B[idx];
+                        else x = reinterpret_cast<const uint16_t *>(B)[idx];
                     }
                     w[(e * E) >> 2] |= x << (8 * ((e * E) & 3));
                 }
@@ -469,7 +473,7 @@ void gemm_tile_kernel(KernelArgs args) {
 #pragma unroll
             for (int i = 0; i < T::B_CHUNKS; ++i) {
                 const int q = i * T::THREADS + tid;
-                const int n = q % BN, c = q / BN;
+                const int n = BT ? q >> 3 : q % BN, c = BT ? q & 7 : q / BN;
                 *reinterpret_cast<u32x4_t *>(bs + n * kStageKBytes + swz(c, n) * 16) = rbc[i];
             }
         }
@@ -784,7 +788,7 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, uint8_t 
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LDS_AS void *)lds_wave_base, 16, int(voff), 0, 0, 0);
 }
 
-template <int DT, int BM, int BN, int WM, int WN, int WAVES_PER_EU>
+template <int DT, int BM, int BN, int WM, int WN, int WAVES_PER_EU, bool BT = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WM * WN, 64 * WM * WN),
                           amdgpu_waves_per_eu(WAVES_PER_EU, WAVES_PER_EU)))
 void gemm_lds_kernel(KernelArgs args) {
@@ -797,8 +801,10 @@ void gemm_lds_kernel(KernelArgs args) {
     constexpr int WAVES = WM * WN;
     constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
     constexpr int A_STAGE = BM * kStageKBytes;            // bytes
-    constexpr int B_PITCH = BN * E;                       // bytes per B row in LDS
-    constexpr int B_STAGE = BK * B_PITCH;                 // == BN * 128
+    // Row-major B sits in LDS as BK rows (k) of BN*E bytes; column-major B (BT)
+    // as BN rows (n) of 128 K-bytes, exactly like A.
+    constexpr int B_PITCH = BT ? kStageKBytes : BN * E;   // bytes per B row in LDS
+    constexpr int B_STAGE = BN * kStageKBytes;
     constexpr int A_INSTR = A_STAGE / 1024 / WAVES;       // 1 KiB per wave-wide load
     constexpr int B_INSTR = B_STAGE / 1024 / WAVES;
     constexpr int B_ROWS_PER_KB = 1024 / B_PITCH;         // B rows covered by one wave-wide load
@@ -849,17 +855,36 @@ void gemm_lds_kernel(KernelArgs args) {
     // writes physical chunk p = L % B_CPR of row (i*WAVES+wave)*B_ROWS_PER_KB + L / B_CPR,
     // holding logical chunk p ^ bswz(row).  Columns at or past N get an out-of-range
     // offset; K rows past the slice end are masked by the resource size.
+    // Column-major B (BT): the same scheme as A over BN rows (n) of the N x K
+    // matrix; rows at or past N are masked by the resource size.
     constexpr int B_CPR = B_PITCH / 16;                   // chunks per B row
-    static_assert(B_CPR >= 16, "transpose-read swizzle needs rows of at least 16 chunks");
+    static_assert(BT || B_CPR >= 16, "transpose-read swizzle needs rows of at least 16 chunks");
+    const int64_t b_rows_valid = (N - n0) < BN ? (N - n0) : BN;
+    const uint32_t bt_bytes = uint32_t(b_rows_valid * ldb_b);
     uint32_t b_voff[B_INSTR];
+    int b_chunk[B_INSTR];
 #pragma unroll
     for (int i = 0; i < B_INSTR; ++i) {
-        const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
-        const int c = (lane % B_CPR) ^ bswz<DT>(row);
-        b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
+        if constexpr (BT) {
+            const int row = (i * WAVES + wave) * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+            b_chunk[i] = c;
+            b_voff[i] = uint32_t(row * ldb_b + c * 16);
+        } else {
+            const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
+            const int c = (lane % B_CPR) ^ bswz<DT>(row);
+            b_chunk[i] = 0;
+            b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
+        }
     }
     const uint8_t *const a_base = static_cast<const uint8_t *>(args.A) + (m0 * args.lda + k_begin) * E;
-    const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
+    const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) +
+                                  (BT ? n0 * args.ldb + k_begin : k_begin * args.ldb + n0) * E;
+    // B resource of stage kt; `rows` valid K rows bound row-major B only.
+    auto b_rsrc = [&](int kt, int64_t rows) {
+        if constexpr (BT) return make_rsrc(b_base + int64_t(kt) * kStageKBytes, bt_bytes);
+        else return make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+    };
     const int64_t k_len = k_end - k_begin;
 
     // Issues the loads of stage kt into LDS buffer BUF.  Full stages use the
@@ -870,7 +895,7 @@ void gemm_lds_kernel(KernelArgs args) {
         const int64_t rem = k_len - int64_t(kt) * BK;
         const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
         const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
-        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+        const __amdgpu_buffer_rsrc_t rb = b_rsrc(kt, rows);
         uint8_t *const as = BUF ? a_lds1 : a_lds0;
         uint8_t *const bs = BUF ? b_lds1 : b_lds0;
         if (rem >= BK) {
@@ -888,7 +913,11 @@ void gemm_lds_kernel(KernelArgs args) {
                 load_lds16(ra, as + (i * WAVES + wave) * 1024, off);
             }
 #pragma unroll
-            for (int i = 0; i < B_INSTR; ++i) load_lds16(rb, bs + (i * WAVES + wave) * 1024, b_voff[i]);
+            for (int i = 0; i < B_INSTR; ++i) {
+                // Column-major B masks its K tail per chunk, as A does; row-major B by rows.
+                const uint32_t off = (!BT || int64_t(b_chunk[i]) * VECE < rem) ? b_voff[i] : kOOB;
+                load_lds16(rb, bs + (i * WAVES + wave) * 1024, off);
+            }
         }
     };
 
@@ -904,7 +933,7 @@ void gemm_lds_kernel(KernelArgs args) {
             return;
         }
         const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, a_bytes);
-        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(BK * ldb_b));
+        const __amdgpu_buffer_rsrc_t rb = b_rsrc(kt, BK);
         uint8_t *const as = BUF ? a_lds1 : a_lds0;
         uint8_t *const bs = BUF ? b_lds1 : b_lds0;
 #pragma unroll
@@ -947,6 +976,14 @@ void gemm_lds_kernel(KernelArgs args) {
         const int colb = (wcol0 + j * 32) * E + tr_colb;
         b_fo[j] = (tr_khalf + tr_row) * B_PITCH + (((colb >> 4) ^ bz) << 4) + (colb & 15);
     }
+    // Column-major B: fragments are 16-byte reads of K-contiguous rows, as for A.
+    const int rb0 = wcol0 + frag_row;
+    const int fb0 = (rb0 ^ (rb0 >> 3)) & 7;
+    int bt_fo[2][4];
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int st = 0; st < 4; ++st) bt_fo[p][st] = rb0 * kStageKBytes + 16 * ((2 * st + frag_half) ^ fb0 ^ (4 * p));
 
     u32x4_t fa[2][TM], fb[2][TN];
     auto load_frags = [&](auto buf_c, auto s_c, auto slot_c) {
@@ -960,9 +997,13 @@ void gemm_lds_kernel(KernelArgs args) {
             fa[SLOT][i] = *reinterpret_cast<const u32x4_t *>(as + a_fo[i & 1][S] + 4096 * i);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const u32x2_t lo = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP) * B_PITCH);
-            const u32x2_t hi = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP + TR_ROWS) * B_PITCH);
-            fb[SLOT][j] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+            if constexpr (BT) {
+                fb[SLOT][j] = *reinterpret_cast<const u32x4_t *>(bs + bt_fo[j & 1][S] + 4096 * j);
+            } else {
+                const u32x2_t lo = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP) * B_PITCH);
+                const u32x2_t hi = lds_read_tr<DT>(bs + b_fo[j] + (S * KSTEP + TR_ROWS) * B_PITCH);
+                fb[SLOT][j] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+            }
         }
     };
 
@@ -1449,13 +1490,40 @@ static hipError_t launch_tile(const KernelArgs &a, int64_t grid, hipStream_t str
 
 template <int DT, int BM, int BN, int WM, int WN, int WPE>
 static hipError_t launch_direct(const KernelArgs &a, int64_t grid, hipStream_t stream) {
-    hipLaunchKernelGGL((gemm_lds_kernel<DT, BM, BN, WM, WN, WPE>), dim3(unsigned(grid)), dim3(64 * WM * WN), 0,
-                       stream, a);
+    if (a.b_trans)
+        hipLaunchKernelGGL((gemm_lds_kernel<DT, BM, BN, WM, WN, WPE, true>), dim3(unsigned(grid)),
+                           dim3(64 * WM * WN), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_lds_kernel<DT, BM, BN, WM, WN, WPE, false>), dim3(unsigned(grid)),
+                           dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
+}
+
+// Column-major B (stored N x K): the element-wise generic kernel and the
+// direct-to-LDS kernel, whose B tile then has A's layout.
+template <int DT>
+static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t grid, hipStream_t s) {
+    switch (cfg) {
+        case 0:
+            hipLaunchKernelGGL((gemm_tile_kernel<DT, 64, 64, 2, 2, false, 2, true>), dim3(unsigned(grid)),
+                               dim3(256), 0, s, a);
+            return hipGetLastError();
+        case 1:
+            hipLaunchKernelGGL((gemm_tile_kernel<DT, 128, 128, 2, 2, false, 1, true>), dim3(unsigned(grid)),
+                               dim3(256), 0, s, a);
+            return hipGetLastError();
+        case 8: return launch_direct<DT, 256, 256, 2, 2, 1>(a, grid, s);
+        case 9: return launch_direct<DT, 128, 256, 2, 2, 1>(a, grid, s);
+        case 10: return launch_direct<DT, 256, 256, 2, 4, 2>(a, grid, s);
+        case 11: return launch_direct<DT, 256, 256, 4, 2, 2>(a, grid, s);
+        case 12: return launch_direct<DT, 128, 256, 2, 4, 2>(a, grid, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int DT>
 static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, hipStream_t s) {
+    if (a.b_trans) return launch_config_bt<DT>(cfg, a, grid, s);
     switch (cfg) {
         case 0: return launch_tile<DT, 64, 64, 2, 2, false, 2>(a, grid, s);
         case 1: return launch_tile<DT, 128, 128, 2, 2, false, 1>(a, grid, s);

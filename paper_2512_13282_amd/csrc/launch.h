@@ -20,6 +20,7 @@ struct KernelArgs {
     int32_t tiles_m, tiles_n;      // output tiles along M and N
     int32_t group_m;               // tile-rows per group in the launch order
     int32_t reduce_in_kernel;      // split-K: 1 = last slice of each tile sums it, 0 = separate kernel
+    int32_t b_trans;               // 1: B is stored column-major (N x K, row stride ldb >= K)
 };
 
 enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2 };

@@ -30,18 +30,21 @@ static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 bool vector_loads_ok(const Problem &p) {
     // 16-byte pieces of A rows and B rows must start 16-byte aligned and never
     // straddle the end of a row; buffer offsets are 32-bit, so a 256-row panel
-    // of either operand must span less than 2 GiB.
+    // of either operand must span less than 2 GiB.  Rows of A and of a
+    // column-major B hold K elements, rows of a row-major B hold N.
     const int64_t e = elem_bytes(p.dtype);
     const int64_t max_row_bytes = int64_t(1) << 22;
+    const int64_t b_row_elems = p.trans_b ? p.K : p.N;
     return (p.a_addr % 16 == 0) && (p.b_addr % 16 == 0) &&
            ((p.lda * e) % 16 == 0) && ((p.ldb * e) % 16 == 0) &&
-           ((p.K * e) % 16 == 0) && ((p.N * e) % 16 == 0) &&
+           ((p.K * e) % 16 == 0) && ((b_row_elems * e) % 16 == 0) &&
            p.lda * e <= max_row_bytes && p.ldb * e <= max_row_bytes;
 }
 
 bool config_applicable(const Problem &p, int32_t cfg) {
     if (cfg < 0 || cfg >= kNumConfigs) return false;
     const TileConfig &c = kConfigs[cfg];
+    if (p.trans_b && !c.col_major_b) return false;
     if (c.family == FAM_GENERIC) return true;
     return vector_loads_ok(p);
 }
@@ -119,7 +122,7 @@ static const TunedPlan kTuned[] = {
 
 bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce) {
     for (const TunedPlan &t : kTuned) {
-        if (t.dtype == p.dtype && t.M == p.M && t.N == p.N && t.K == p.K &&
+        if (!p.trans_b && t.dtype == p.dtype && t.M == p.M && t.N == p.N && t.K == p.K &&
             t.config >= 0 && t.config < kNumConfigs && config_applicable(p, t.config)) {
             *config = t.config;
             *split = t.split;

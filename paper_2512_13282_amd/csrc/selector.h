@@ -12,6 +12,7 @@ struct Problem {
     int64_t M, N, K;
     int64_t lda, ldb, ldc;
     uintptr_t a_addr, b_addr, c_addr;
+    int32_t trans_b = 0;   // 1: B stored column-major (N x K, row stride ldb)
 };
 
 struct Plan {

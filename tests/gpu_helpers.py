@@ -81,6 +81,28 @@ def check_bf16(A: np.ndarray, B: np.ndarray, C: np.ndarray) -> None:
     assert err <= BF16_TOL, err
 
 
+def call_bt(dtype: int, M: int, N: int, K: int, A, lda, Bt, ldbt, C, ldc) -> int:
+    fn = b.gemm_i8_i32_bt if dtype == I8 else b.gemm_bf16_f32_bt
+    stream = torch.cuda.current_stream().cuda_stream
+    return fn(M, N, K, A.data_ptr(), lda, Bt.data_ptr(), ldbt, C.data_ptr(), ldc, stream)
+
+
+def gemm_gpu_bt(dtype: int, A: np.ndarray, Bt: np.ndarray, pad=(0, 0, 0)) -> np.ndarray:
+    """Runs the column-major-B entry point (Bt is N x K) and returns C (M x N) as numpy."""
+    M, K = A.shape
+    N = Bt.shape[0]
+    dA, lda = to_dev(A, pad[0])
+    dB, ldbt = to_dev(Bt, pad[1])
+    dC, ldc = out_buffer(M, N, dtype, pad[2])
+    rc = call_bt(dtype, M, N, K, dA, max(lda, 1), dB, max(ldbt, 1), dC, max(ldc, 1))
+    assert rc == b.GEMM_OK, b.gemm_status_string(rc)
+    torch.cuda.synchronize()
+    host = dC.cpu().numpy()
+    if M == 0 or N == 0:
+        return np.zeros((M, N), host.dtype)
+    return host[: M * ldc].reshape(M, ldc)[:, :N]
+
+
 def force(dtype: int, kernel: int = b.GEMM_KERNEL_AUTO, config: int = -1, split: int = 0,
           reduce: int = -1) -> None:
     assert b.gemm_force_plan(dtype, kernel, config, split) == b.GEMM_OK

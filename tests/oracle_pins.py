@@ -300,4 +300,43 @@ def pin_bf16_sequential_order(o):
             assert C[i, j] == s
 
 
+# ----------------------------------------------------------------------------- column-major B
+def pin_i8_bt_bruteforce_tiny(o):
+    """C = A Bt^T with Bt stored N x K: all (M, N, K) in {0..3}^3 (square shapes included,
+    where a missing transpose would still type-check) against Python big-int sums."""
+    rng = RNG(61)
+    for M in range(4):
+        for N in range(4):
+            for K in range(4):
+                A = rng.integers(-128, 128, size=(M, K), dtype=np.int8)
+                Bt = rng.integers(-128, 128, size=(N, K), dtype=np.int8)
+                C, ovf = o.gemm_i8_i32_bt(A, Bt)
+                assert ovf == 0 and C.shape == (M, N)
+                for i in range(M):
+                    for j in range(N):
+                        exact = sum(int(A[i, k]) * int(Bt[j, k]) for k in range(K))
+                        assert int(C[i, j]) == exact, (M, N, K, i, j)
+    A = rng.integers(-128, 128, size=(6, 9), dtype=np.int8)
+    Bt = rng.integers(-128, 128, size=(5, 9), dtype=np.int8)
+    C = o.gemm_i8_i32_bt(A, Bt)[0]
+    assert o.freivalds_i8_i32_bt(A, Bt, C) == 0
+    C[2, 3] += 1
+    assert o.freivalds_i8_i32_bt(A, Bt, C) > 0
+
+
+def pin_bf16_bt_exact_rational_tiny(o):
+    """bf16 C = A Bt^T on small shapes within the fp64 summation bound of the exact sum."""
+    rng = RNG(62)
+    for (M, N, K) in ((1, 1, 1), (3, 3, 3), (2, 5, 4), (4, 2, 7)):
+        A = inputs.bf16_bits_from_f32(rng.standard_normal((M, K), dtype=np.float32) * 3)
+        Bt = inputs.bf16_bits_from_f32(rng.standard_normal((N, K), dtype=np.float32) * 3)
+        C = o.gemm_bf16_f64_bt(A, Bt)
+        for i in range(M):
+            for j in range(N):
+                terms = [_frac_bf16(int(A[i, k])) * _frac_bf16(int(Bt[j, k])) for k in range(K)]
+                exact = sum(terms, Fraction(0))
+                bound = max(K - 1, 0) * Fraction(1, 2 ** 53) * sum(abs(t) for t in terms)
+                assert abs(Fraction(float(C[i, j])) - exact) <= bound, (M, N, K, i, j)
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

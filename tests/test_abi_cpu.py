@@ -94,3 +94,25 @@ def test_plan_invalid_arguments():
         b.gemm_plan(I8, 4, 4, 4, 3, 4, 4, FAKE_A, FAKE_B, FAKE_C)
     with pytest.raises(b.GemmError):
         b.gemm_plan(5, 4, 4, 4, 4, 4, 4, FAKE_A, FAKE_B, FAKE_C)
+
+
+@pytest.mark.parametrize("fn", [b.gemm_i8_i32_bt, b.gemm_bf16_f32_bt])
+@pytest.mark.parametrize("args", [
+    (-1, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4),     # negative M
+    (4, 8, 16, FAKE_A, 16, FAKE_B, 15, FAKE_C, 8),   # ldbt < K (Bt is N x K)
+    (4, 4, 4, FAKE_A, 4, 0, 4, FAKE_C, 4),           # null Bt
+    (4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_B + 4, 4),  # C overlaps Bt
+    (4, 4, 4, FAKE_A, 4, FAKE_B, 1 << 62, FAKE_C, 4),  # stride overflow
+])
+def test_bt_invalid_arguments_rejected_before_hip(fn, args):
+    assert fn(*args, 0) == b.GEMM_ERR_INVALID_VALUE
+
+
+def test_bt_strides_follow_the_n_by_k_layout():
+    # Bt is N x K: a row stride >= K is valid even when it is < N, which the row-major
+    # entry point (rows of N) rejects
+    p = b.gemm_plan(I8, 64, 512, 128, 128, 128, 512, FAKE_A, FAKE_B, FAKE_C, trans_b=True)
+    assert p["split_k"] >= 1
+    with pytest.raises(b.GemmError):
+        b.gemm_plan(I8, 64, 512, 128, 128, 128, 512, FAKE_A, FAKE_B, FAKE_C)
+    assert b.gemm_i8_i32_bt(0, 5, 7, 0, 7, FAKE_B, 7, 0, 5, 0) == b.GEMM_OK

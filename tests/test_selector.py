@@ -169,3 +169,37 @@ def test_split_k_reduction_choice():
     finally:
         b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
         b.gemm_force_reduce(I8, -1)
+
+
+def plan_bt(dtype, M, N, K, ldbt=None, off=0):
+    return b.gemm_plan(dtype, M, N, K, max(K, 1), ldbt or max(K, 1), max(N, 1), AL + off, 2 * AL, 3 * AL,
+                       trans_b=True)
+
+
+@pytest.mark.parametrize("dtype", [I8, BF])
+def test_column_major_b_plans(dtype):
+    """B stored N x K runs on the configurations built for it (the generic and direct
+    families), with the same tiling invariants; alignment of Bt rows is judged on K."""
+    for M, N, K in itertools.product([1, 17, 64, 257, 4096], [1, 8, 33, 256, 4000], [0, 1, 16, 100, 8192]):
+        p = plan_bt(dtype, M, N, K)
+        check_invariants(p, dtype, M, N, K)
+        assert p["kernel"] in (b.GEMM_KERNEL_GENERIC, b.GEMM_KERNEL_DIRECT)
+        assert not p["name"].startswith("pingpong")
+    # N need not be a multiple of 16 bytes for column-major B, K must
+    assert plan_bt(dtype, 512, 4100, 4096)["kernel"] == b.GEMM_KERNEL_DIRECT
+    assert plan_bt(dtype, 512, 512, 4097)["kernel"] == b.GEMM_KERNEL_GENERIC
+    assert plan_bt(dtype, 512, 512, 4096, off=ESZ[dtype])["kernel"] == b.GEMM_KERNEL_GENERIC
+    big = plan_bt(dtype, 8192, 8192, 8192)
+    assert big["kernel"] == b.GEMM_KERNEL_DIRECT and big["bm"] == 256 and big["bn"] == 256
+
+
+def test_column_major_b_rejects_configs_without_it():
+    try:
+        for cfg in (2, 6, 13, 14):
+            assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, cfg, 1) == b.GEMM_OK
+            with pytest.raises(b.GemmError) as e:
+                plan_bt(I8, 512, 512, 4096)
+            assert e.value.status == b.GEMM_ERR_UNSUPPORTED
+            plan(I8, 512, 512, 4096)      # the row-major form still runs it
+    finally:
+        b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
