@@ -46,6 +46,7 @@ def parse():
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bt", action="store_true", help="skip the column-major-B measurements")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the sustained-MFMA-ceiling probe")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--only", choices=["int8", "bf16"], default=None)
     ap.add_argument("--config", type=int, default=-1,
@@ -208,6 +209,38 @@ def cpu_baseline(w: Workload, seconds: float):
                       f"({rows * w.N} outputs, {ops:.3g} ops)"}
 
 
+def mfma_ceiling(dtype: str, iters: int = 20000, launches: int = 3) -> dict:
+    """Sustained MFMA rate with random operands in registers and no memory traffic
+    (gemm_probe_mfma): the ceiling a GEMM on random inputs can reach at the clock the
+    chip holds under that load.  Timed with HIP events on the launch stream."""
+    import torch
+    from paper_2512_13282_amd import binding
+    d = binding.GEMM_DTYPE_I8_I32 if dtype == "int8" else binding.GEMM_DTYPE_BF16_F32
+    rc, info = binding.gemm_probe_mfma(d, True, iters)
+    if rc != 0:
+        raise RuntimeError(binding.gemm_status_string(rc))
+    wg = int(info["workgroups"])
+    clocks = torch.zeros(2 * wg, dtype=torch.int64, device="cuda:0")
+    sink = torch.zeros(wg * int(info["threads_per_workgroup"]), dtype=torch.int32, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    ms = []
+    for i in range(launches + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        rc, _ = binding.gemm_probe_mfma(d, True, iters, clocks.data_ptr(), sink.data_ptr(), stream.cuda_stream)
+        e1.record(stream)
+        if rc != 0:
+            raise RuntimeError(binding.gemm_status_string(rc))
+        torch.cuda.synchronize()
+        if i > 0:
+            ms.append(e0.elapsed_time(e1))
+    c = clocks.view(wg, 2).double().cpu()
+    ghz = float((c[:, 0] / c[:, 1]).mean()) * info["wall_clock_hz"] / 1e9
+    tops = info["ops_per_launch"] / (float(np.mean(ms)) * 1e-3) / 1e12
+    return {"value": round(tops, 1), "unit": "TOPS" if dtype == "int8" else "TFLOP/s",
+            "clock_ghz": round(ghz, 3), "frac_of_published_peak": round(tops / PEAK[dtype], 4)}
+
+
 def write_traffic(fetch_csv: str, write_csv: str) -> None:
     """HBM bytes per launch of the timed GEMM kernels from rocprofv3 counter CSVs.
 
@@ -342,6 +375,16 @@ def main():
                 del w
                 torch.cuda.empty_cache()
 
+    ceiling = {}
+    if not args.no_ceiling:
+        for dtype in results:
+            ceiling[dtype] = mfma_ceiling(dtype)
+            ceiling[dtype]["gemm_frac_of_ceiling"] = round(results[dtype][1]["roofline"]["achieved"] /
+                                                           ceiling[dtype]["value"], 4)
+            print(f"[bench] {dtype} sustained MFMA ceiling (random operands, no memory traffic): "
+                  f"{ceiling[dtype]['value']} at {ceiling[dtype]['clock_ghz']} GHz; GEMM kernel reaches "
+                  f"{ceiling[dtype]['gemm_frac_of_ceiling']:.3f} of it", file=sys.stderr, flush=True)
+
     head_dtype = args.only or "int8"
     hw, hr = results[head_dtype]
     line = {
@@ -365,6 +408,10 @@ def main():
         if dtype != head_dtype:
             line[dtype] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg", "pct_dense_peak",
                                             "plan", "split_k", "parity_sample_ok", "roofline")}
+    if ceiling:
+        line["mfma_ceiling"] = {"method": "gemm_probe_mfma: only the GEMM's MFMA instructions on random "
+                                          "operands held in registers, one 8-wave workgroup per CU, no memory "
+                                          "traffic; HIP-event timed", **ceiling}
     if bt_results:
         line["column_major_b"] = {"workload": f"the same GEMMs with B stored column-major (N x K), "
                                               f"gemm_*_bt entry points", **bt_results}

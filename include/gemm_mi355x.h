@@ -169,6 +169,34 @@ int gemm_force_plan(int dtype, int kernel, int config, int split_k);
  * Returns GEMM_OK, or GEMM_ERR_HIP if a synchronization or free failed. */
 int gemm_release_workspace(void);
 
+/* ---- Measurement aid (not part of the GEMM) ------------------------------
+ * gemm_probe_mfma runs one workgroup of 8 waves per compute unit that issues
+ * only the GEMM's 32x32 MFMA instructions (int8 32x32x32 or bf16 32x32x16,
+ * chosen by `dtype`) for `iters` iterations of 32 MFMAs per wave, on operands
+ * held in registers: random data shaped like the GEMM inputs (int8 uniform
+ * bytes, bf16 approximately N(0,1)) when `random_operands` is non-zero,
+ * constants otherwise.  No memory traffic occurs inside the loop, so ops per
+ * launch divided by the launch's duration is the MFMA ceiling at the clock the
+ * chip sustains under that load; the MI355X clock falls well below its maximum
+ * when the multipliers see random data.
+ *
+ * `clocks` (device, 2 * workgroups int64) receives per workgroup the
+ * shader-clock cycles and the constant-rate wall-clock ticks spent in the
+ * loop; their ratio times wall_clock_hz is the clock the loop ran at.  `sink`
+ * (device, workgroups * threads_per_workgroup uint32) receives values that keep
+ * the results live.  With clocks == sink == NULL only `info` is filled.
+ * Asynchronous on `stream`.  Returns GEMM_OK, GEMM_ERR_INVALID_VALUE (bad dtype,
+ * iters < 1, info NULL, only one of the buffers given) or GEMM_ERR_HIP. */
+typedef struct gemm_probe_info {
+    int64_t workgroups;            /* one per compute unit                    */
+    int64_t threads_per_workgroup;
+    double  ops_per_launch;        /* 2 * multiply-adds of all MFMAs          */
+    double  wall_clock_hz;         /* rate of the wall-clock ticks in clocks  */
+} gemm_probe_info;
+
+int gemm_probe_mfma(int dtype, int random_operands, int32_t iters, int64_t *clocks,
+                    unsigned *sink, gemm_probe_info *info, void *stream);
+
 /* Static description of the error code. */
 const char *gemm_status_string(int status);
 

@@ -3,7 +3,7 @@
 The functions named like the C entry points (``gemm_i8_i32``, ``gemm_bf16_f32``,
 their column-major-B forms ``gemm_i8_i32_bt`` and ``gemm_bf16_f32_bt``, ``gemm_plan``,
 ``gemm_plan_bt``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
-``gemm_status_string``, ``gemm_version``)
+``gemm_status_string``, ``gemm_version``, and the measurement aid ``gemm_probe_mfma``)
 take plain integers and device addresses exactly as the C ABI does.  The two
 torch helpers (``mm_i8_i32``, ``mm_bf16_f32``) only read ``data_ptr()``,
 strides and the current HIP stream of torch tensors and call the same entry
@@ -35,7 +35,7 @@ GEMM_KERNEL_DIRECT = 3
 
 EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt", "gemm_plan",
             "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",
-            "gemm_status_string", "gemm_version")
+            "gemm_status_string", "gemm_version", "gemm_probe_mfma")
 
 
 class PlanInfo(ctypes.Structure):
@@ -51,6 +51,11 @@ class PlanInfo(ctypes.Structure):
         ("model_t_comp_us", ctypes.c_double), ("model_t_mem_us", ctypes.c_double),
         ("name", ctypes.c_char * 48),
     ]
+
+
+class ProbeInfo(ctypes.Structure):
+    _fields_ = [("workgroups", ctypes.c_int64), ("threads_per_workgroup", ctypes.c_int64),
+                ("ops_per_launch", ctypes.c_double), ("wall_clock_hz", ctypes.c_double)]
 
 
 class GemmError(RuntimeError):
@@ -96,6 +101,8 @@ def lib() -> ctypes.CDLL:
         l.gemm_status_string.restype = ctypes.c_char_p
         l.gemm_version.argtypes = []
         l.gemm_version.restype = ctypes.c_char_p
+        l.gemm_probe_mfma.argtypes = [i32, i32, ctypes.c_int32, p, p, ctypes.POINTER(ProbeInfo), p]
+        l.gemm_probe_mfma.restype = i32
         _lib = l
     return _lib
 
@@ -148,6 +155,14 @@ def gemm_status_string(status: int) -> str:
 
 def gemm_version() -> str:
     return lib().gemm_version().decode()
+
+
+def gemm_probe_mfma(dtype, random_operands, iters, clocks=0, sink=0, stream=0):
+    """Returns (status, info dict); with clocks == sink == 0 only the info is filled."""
+    info = ProbeInfo()
+    rc = lib().gemm_probe_mfma(dtype, int(bool(random_operands)), iters, clocks or None, sink or None,
+                               ctypes.byref(info), stream or None)
+    return rc, {f: getattr(info, f) for f, _ in ProbeInfo._fields_}
 
 
 # ---------------------------------------------------------------- torch helpers

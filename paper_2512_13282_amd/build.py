@@ -21,7 +21,7 @@ LIB = os.path.join(PKG, "libgemm_mi355x.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HOST_SOURCES = ["gemm_api.cpp", "selector.cpp"]
-DEVICE_SOURCES = ["gemm_kernels.hip"]
+DEVICE_SOURCES = ["gemm_kernels.hip", "mfma_probe.hip"]
 
 # Packed-fp32 instructions are disabled for all device code (the hipcc host
 # pass warns that it does not know the feature; that warning is harmless).
