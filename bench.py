@@ -63,16 +63,16 @@ def kernel_sha() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
 
 
-def traffic_for(dtype: str, M: int, N: int, K: int):
+def traffic_for(dtype: str, M: int, N: int, K: int, bt: bool = False):
     """HBM bytes per launch from committed rocprofv3 FETCH_SIZE/WRITE_SIZE counters, or None
-    when none were taken for this workload or the kernel source changed since."""
+    when none were taken for this workload (B layout included) or the kernel source changed since."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     if t.get("kernel_source_sha256") != kernel_sha():
         return None
-    rec = t.get("workloads", {}).get(f"{dtype}_{M}x{K}x{N}")
+    rec = t.get("workloads", {}).get(f"{dtype}_{M}x{K}x{N}" + ("_bt" if bt else ""))
     return None if rec is None else rec.get("bytes_per_launch")
 
 
@@ -142,7 +142,7 @@ def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
     value = ops / (ms_step * 1e-3) / 1e12
     achieved = ops / (k_avg * 1e-3) / 1e12
     mem_bound = ops / comp_bytes < (PEAK[w.dtype] * 1e12) / (HBM_GBS * 1e9)
-    traffic = traffic_for(w.dtype, w.M, w.N, w.K)
+    traffic = traffic_for(w.dtype, w.M, w.N, w.K, w.bt)
     if mem_bound:
         ach_gbs = comp_bytes / (k_avg * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach_gbs, 1), "peak": HBM_GBS, "unit": "GB/s",
@@ -276,14 +276,17 @@ def write_traffic(fetch_csv: str, write_csv: str) -> None:
     S = 8192
     workloads = {}
     for k in fetch:
-        if "gemm::" not in k:
+        # gemm_lds_kernel<dtype, BM, BN, WM, WN, waves/EU, B column-major>: one plan per workload
+        if "gemm::gemm_lds_kernel<" not in k:
             continue
-        dtype = "int8" if "<0," in k else "bf16"
+        targs = [t.strip() for t in k.split("<", 1)[1].split(">", 1)[0].split(",")]
+        dtype = "int8" if targs[0] == "0" else "bf16"
+        bt = targs[-1] == "true"
         e = 1 if dtype == "int8" else 2
         comp = S * S * e * 2 + S * S * 4
         fb = fetch[k] * 1024.0 * f_scale
         wb = write.get(k, 0.0) * 1024.0 * w_scale
-        workloads[f"{dtype}_{S}x{S}x{S}"] = {
+        workloads[f"{dtype}_{S}x{S}x{S}" + ("_bt" if bt else "")] = {
             "kernel": k, "fetch_bytes": round(fb), "write_bytes": round(wb),
             "bytes_per_launch": round(fb + wb), "algorithmic_bytes": comp,
             "traffic_over_algorithmic": round((fb + wb) / comp, 3)}
