@@ -78,7 +78,8 @@ typedef enum {
     GEMM_KERNEL_GENERIC = 0, /* any alignment; element-wise masked loads       */
     GEMM_KERNEL_MACRO = 1,   /* 16-byte vector loads, large LDS macro-tiles    */
     GEMM_KERNEL_SKINNY = 2,  /* small M: narrow M tile, wide N, split-K        */
-    GEMM_KERNEL_DIRECT = 3   /* global -> LDS direct loads, LDS transpose reads */
+    GEMM_KERNEL_DIRECT = 3,  /* global -> LDS direct loads, LDS transpose reads */
+    GEMM_KERNEL_RING = 4     /* as DIRECT, 64-byte K slots in a deeper LDS ring */
 } gemm_kernel_t;
 
 /* The selector's choice for one call (filled by gemm_plan). */

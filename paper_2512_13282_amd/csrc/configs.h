@@ -19,7 +19,7 @@ namespace gemm {
 
 enum Dtype : int32_t { DT_I8 = 0, DT_BF16 = 1 };
 
-enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2, FAM_DIRECT = 3 };
+enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2, FAM_DIRECT = 3, FAM_RING = 4 };
 
 struct TileConfig {
     int32_t family;
@@ -37,6 +37,10 @@ struct TileConfig {
 // elements.  Every MFMA consumes 32 bytes of K per lane pair (bf16 32x32x16,
 // int8 32x32x32), so a stage is 4 MFMA k-steps.
 constexpr int32_t kStageKBytes = 128;
+
+// The ring family walks K in 64-byte slots (two MFMA k-steps), `stages` of them
+// resident in LDS at once.
+constexpr int32_t kSlotKBytes = 64;
 
 // Family GENERIC: alignment-agnostic element-wise loads (any lda/ldb/K/N).
 // Family MACRO: 16-byte vector loads staged through registers (B transposed
@@ -63,6 +67,10 @@ constexpr TileConfig kConfigs[] = {
     {FAM_DIRECT,   256, 256, 2, 4, 1, 2, 0.30, 0.30, 0, "pingpong_256x256_w8"},
     {FAM_SKINNY,    32, 256, 1, 4, 1, 4, 0.10, 0.12, 0, "stream_32x256_s4"},
     {FAM_SKINNY,    64, 256, 1, 4, 1, 3, 0.15, 0.18, 0, "stream_64x256_s3"},
+    {FAM_RING,     256, 256, 2, 4, 1, 4, 0.40, 0.45, 1, "ring_256x256_w8"},
+    {FAM_RING,     256, 256, 4, 2, 1, 4, 0.40, 0.45, 1, "ring_256x256_w8t"},
+    {FAM_RING,     128, 256, 2, 4, 1, 5, 0.38, 0.34, 1, "ring_128x256_w8"},
+    {FAM_RING,     256, 256, 2, 2, 1, 4, 0.38, 0.42, 1, "ring_256x256_w4"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 
@@ -70,7 +78,7 @@ constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 // B stage (bn x 128 B).  The analog of the paper's L1 budget (Eq. 5) without
 // the C term: the output tile lives in registers, not in LDS.
 constexpr int64_t lds_bytes(const TileConfig &c) {
-    return int64_t(c.stages) * (int64_t(c.bm) + int64_t(c.bn)) * kStageKBytes;
+    return int64_t(c.stages) * (int64_t(c.bm) + int64_t(c.bn)) * (c.family == FAM_RING ? kSlotKBytes : kStageKBytes);
 }
 
 }  // namespace gemm

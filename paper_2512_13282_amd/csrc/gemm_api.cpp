@@ -228,7 +228,7 @@ int gemm_plan_bt(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_
 int gemm_force_plan(int dtype, int kernel, int config, int split_k) {
     if (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32) return GEMM_ERR_INVALID_VALUE;
     if (split_k < 0 || config < -1 || config >= gemm::kNumConfigs) return GEMM_ERR_INVALID_VALUE;
-    if (kernel < GEMM_KERNEL_AUTO || kernel > GEMM_KERNEL_DIRECT) return GEMM_ERR_INVALID_VALUE;
+    if (kernel < GEMM_KERNEL_AUTO || kernel > GEMM_KERNEL_RING) return GEMM_ERR_INVALID_VALUE;
     if (config >= 0 && kernel >= 0 && gemm::kConfigs[config].family != kernel) return GEMM_ERR_INVALID_VALUE;
     std::lock_guard<std::mutex> lk(g_mu);
     Override &o = g_override[dtype];
