@@ -71,6 +71,12 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,     256, 256, 4, 2, 1, 4, 0.40, 0.45, 1, "ring_256x256_w8t"},
     {FAM_RING,     128, 256, 2, 4, 1, 5, 0.38, 0.34, 1, "ring_128x256_w8"},
     {FAM_RING,     256, 256, 2, 2, 1, 4, 0.38, 0.42, 1, "ring_256x256_w4"},
+    {FAM_RING,      32,  64, 1, 2, 2, 8, 0.10, 0.12, 1, "ring_32x64_w2"},
+    {FAM_RING,      64,  64, 1, 2, 2, 8, 0.15, 0.18, 1, "ring_64x64_w2"},
+    {FAM_RING,      32, 128, 1, 4, 1, 8, 0.12, 0.14, 1, "ring_32x128_w4"},
+    {FAM_RING,      64, 128, 1, 4, 1, 8, 0.18, 0.20, 1, "ring_64x128_w4"},
+    {FAM_RING,      32, 256, 1, 4, 1, 6, 0.15, 0.18, 1, "ring_32x256_w4"},
+    {FAM_RING,      64, 256, 1, 4, 1, 6, 0.22, 0.26, 1, "ring_64x256_w4"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

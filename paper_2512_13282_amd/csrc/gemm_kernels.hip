@@ -1098,8 +1098,8 @@ void gemm_lds_kernel(KernelArgs args) {
 // LDS, per slot: A as BM rows of 64 K-bytes, the 16-byte chunk c of row r at
 // chunk c ^ ga(r), ga(r) = ((r >> 1) ^ (r >> 3)) & 3, which keeps the fragment
 // reads of any 8 (and any 16) consecutive rows on distinct banks; B row-major
-// as 64 / E rows (k) of BN * E bytes with gemm_lds_kernel's swizzle, or
-// column-major (BT) like A.  Every slot of every iteration issues the same
+// as 64 / E rows (k) of BN * E bytes with gemm_lds_kernel's swizzle (rows of
+// at least 256 bytes; narrower rows unswizzled), or column-major (BT) like A.  Every slot of every iteration issues the same
 // number of loads (slots past the end of the K range get an empty resource and
 // load zeros without touching memory), so the wait before each barrier is a
 // fixed count of this wave's loads still allowed in flight.
@@ -1117,9 +1117,16 @@ __device__ __forceinline__ i32x4_t ring_rsrc(const uint8_t *base, uint32_t bytes
 // rsrc + voff land at LDS byte lds + 16 l.  Written as inline assembly so that
 // the compiler does not tie the LDS reads that follow to these writes (it cannot
 // tell the ring buffers apart and would wait for every load in flight before each
-// read); completion is tracked by the explicit vmcnt waits of the ring instead.
+// read); completion is tracked by the explicit vmcnt waits of the ring instead,
+// and nothing else in the kernel accesses the ring.
 __device__ __forceinline__ void ring_load16(i32x4_t rsrc, uint32_t lds, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :: "v"(voff), "s"(rsrc), "s"(lds) : "memory", "m0");
+}
+
+// The same with 4 bytes per lane: lane l's dword lands at LDS byte lds + 4 l.
+__device__ __forceinline__ void ring_load4(i32x4_t rsrc, uint32_t lds, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
                  :: "v"(voff), "s"(rsrc), "s"(lds) : "memory", "m0");
 }
 
@@ -1146,35 +1153,31 @@ void gemm_ring_kernel(KernelArgs args) {
     constexpr int A_SLOT = BM * kSlotKBytes;              // bytes
     constexpr int B_PITCH = BT ? kSlotKBytes : BN * E;    // bytes per B row in LDS
     constexpr int B_SLOT = BN * kSlotKBytes;
-    constexpr int A_INSTR = A_SLOT / 1024 / WAVES;        // 1 KiB per wave-wide load
+    // A moves in 16-byte pieces per lane (1 KiB per wave-wide load) when its slot
+    // splits evenly into such loads over the waves, else in 4-byte pieces (256 B per
+    // load); B always moves in 16-byte pieces.
+    constexpr int A_W = (A_SLOT % (1024 * WAVES) == 0) ? 16 : 4;
+    constexpr int A_LOAD = 64 * A_W;                      // bytes per wave-wide A load
+    constexpr int A_INSTR = A_SLOT / A_LOAD / WAVES;
+    constexpr int A_ROWS_PER_LOAD = A_LOAD / kSlotKBytes;
     constexpr int B_INSTR = B_SLOT / 1024 / WAVES;
     constexpr int LPS = A_INSTR + B_INSTR;                // loads per wave per slot
     constexpr int B_ROWS_PER_KB = 1024 / B_PITCH;
     constexpr int B_CPR = B_PITCH / 16;                   // 16-byte chunks per B row
+    // Row-major B rows of 16 or more chunks are swizzled for conflict-free transpose
+    // reads; narrower rows (small BN) are stored as they are.
+    constexpr bool B_SWZ = !BT && B_CPR >= 16;
     constexpr int NREAD = TM + (BT ? TN : 2 * TN);        // LDS reads per k-step
-    static_assert(NB >= 3 && NB <= 5, "ring depth");
-    static_assert(A_INSTR >= 1 && A_INSTR * 1024 * WAVES == A_SLOT, "A slot split");
+    static_assert(NB >= 3 && NB <= 8, "ring depth");
+    static_assert(TM >= 1 && TN >= 1, "wave tile of at least one 32 x 32 MFMA tile");
+    static_assert(A_INSTR >= 1 && A_INSTR * A_LOAD * WAVES == A_SLOT, "A slot split");
     static_assert(B_INSTR >= 1 && B_INSTR * 1024 * WAVES == B_SLOT, "B slot split");
     static_assert(B_PITCH <= 1024 && 1024 % B_PITCH == 0, "B row pitch");
-    static_assert(BT || B_CPR >= 16, "transpose-read swizzle needs rows of at least 16 chunks");
     static_assert((NB - 1) * LPS < 64, "loads in flight must fit vmcnt");
 
-    // One LDS array per ring buffer (A part, then B part), so that the compiler can
-    // tell the direct-to-LDS writes into one buffer from the fragment reads of
-    // another and does not make the reads wait for them.
-    __shared__ __attribute__((aligned(1024))) uint8_t lds0[A_SLOT + B_SLOT];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds1[A_SLOT + B_SLOT];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds2[A_SLOT + B_SLOT];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds3[A_SLOT + B_SLOT];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds4[A_SLOT + B_SLOT];
-    auto abuf = [&](auto j_c) -> uint8_t * {
-        constexpr int J = decltype(j_c)::value;
-        if constexpr (J == 0) return lds0;
-        else if constexpr (J == 1) return lds1;
-        else if constexpr (J == 2) return lds2;
-        else if constexpr (J == 3) return lds3;
-        else return lds4;
-    };
+    // The ring: NB buffers, each an A part then a B part.
+    __shared__ __attribute__((aligned(1024))) uint8_t ring_lds[NB][A_SLOT + B_SLOT];
+    auto abuf = [&](auto j_c) -> uint8_t * { return ring_lds[decltype(j_c)::value]; };
     auto bbuf = [&](auto j_c) -> uint8_t * { return abuf(j_c) + A_SLOT; };
 
     const int tid = threadIdx.x;
@@ -1204,10 +1207,12 @@ void gemm_ring_kernel(KernelArgs args) {
     int a_chunk[A_INSTR];
 #pragma unroll
     for (int i = 0; i < A_INSTR; ++i) {
-        const int row = (i * WAVES + wave) * 16 + (lane >> 2);
-        const int c = (lane & 3) ^ ring_swz(row);
+        // Lane L writes A_W bytes at byte L * A_W of the load's block of A_ROWS_PER_LOAD rows.
+        const int row = (i * WAVES + wave) * A_ROWS_PER_LOAD + (lane * A_W) / kSlotKBytes;
+        const int byte = (lane * A_W) % kSlotKBytes;
+        const int c = (byte >> 4) ^ ring_swz(row);
         a_chunk[i] = c;
-        a_voff[i] = uint32_t(row * lda_b + c * 16);
+        a_voff[i] = uint32_t(row * lda_b + c * 16 + (byte & 15));
     }
     // Row-major B: load i fills B-slot bytes [(i*WAVES + wave) KiB, +1 KiB): lane L writes
     // physical chunk p = L % B_CPR of row (i*WAVES + wave)*B_ROWS_PER_KB + L / B_CPR, holding
@@ -1227,7 +1232,7 @@ void gemm_ring_kernel(KernelArgs args) {
             b_voff[i] = uint32_t(row * ldb_b + c * 16);
         } else {
             const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
-            const int c = (lane % B_CPR) ^ bswz<DT>(row);
+            const int c = (lane % B_CPR) ^ (B_SWZ ? bswz<DT>(row) : 0);
             b_chunk[i] = 0;
             b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
         }
@@ -1236,9 +1241,6 @@ void gemm_ring_kernel(KernelArgs args) {
     const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) +
                                   (BT ? n0 * args.ldb + k_begin : k_begin * args.ldb + n0) * E;
 
-    // Issues the loads of slot kt into ring buffer J.  Full slots use the precomputed
-    // offsets as they are; a partial last slot masks its K tail per chunk (A, and
-    // column-major B) or by rows (row-major B); slots past the end load nothing.
     // Issues load L (A loads first, then B loads) of slot kt into ring buffer J.  A
     // partial last slot masks its K tail per chunk (A, and column-major B) or by rows
     // (row-major B, through the resource size); slots past the end load nothing.
@@ -1248,7 +1250,9 @@ void gemm_ring_kernel(KernelArgs args) {
         if constexpr (L < A_INSTR) {
             const i32x4_t ra = ring_rsrc(a_base + int64_t(kt) * kSlotKBytes, rem > 0 ? a_bytes : 0u);
             const uint32_t off = (rem >= BKS || int64_t(a_chunk[L]) * VECE < rem) ? a_voff[L] : kOOB;
-            ring_load16(ra, lds_addr(abuf(j_c)) + (L * WAVES + wave_u) * 1024, off);
+            const uint32_t dst = lds_addr(abuf(j_c)) + (L * WAVES + wave_u) * A_LOAD;
+            if constexpr (A_W == 16) ring_load16(ra, dst, off);
+            else ring_load4(ra, dst, off);
         } else {
             constexpr int I = L - A_INSTR;
             i32x4_t rb;
@@ -1289,7 +1293,7 @@ void gemm_ring_kernel(KernelArgs args) {
     const int tr_row = DT == DT_BF16 ? (g16 >> 2) : (g16 >> 1);
     const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (grp & 1) * 16 * E;
     const int tr_khalf = (grp >> 1) * (KSTEP / 2);
-    const int bz = bswz<DT>(tr_row);
+    const int bz = B_SWZ ? bswz<DT>(tr_row) : 0;
     int b_fo[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -1854,6 +1858,12 @@ static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t gri
         case 17: return launch_ring<DT, 256, 256, 4, 2, 2, 4>(a, grid, s);
         case 18: return launch_ring<DT, 128, 256, 2, 4, 2, 5>(a, grid, s);
         case 19: return launch_ring<DT, 256, 256, 2, 2, 1, 4>(a, grid, s);
+        case 20: return launch_ring<DT, 32, 64, 1, 2, 2, 8>(a, grid, s);
+        case 21: return launch_ring<DT, 64, 64, 1, 2, 2, 8>(a, grid, s);
+        case 22: return launch_ring<DT, 32, 128, 1, 4, 2, 8>(a, grid, s);
+        case 23: return launch_ring<DT, 64, 128, 1, 4, 2, 8>(a, grid, s);
+        case 24: return launch_ring<DT, 32, 256, 1, 4, 1, 6>(a, grid, s);
+        case 25: return launch_ring<DT, 64, 256, 1, 4, 1, 6>(a, grid, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1884,7 +1894,8 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
         case 15:
             hipLaunchKernelGGL((gemm_stream_kernel<DT, 64, 3>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
-        case 16: case 17: case 18: case 19: return launch_config_bt<DT>(cfg, a, grid, s);
+        case 16: case 17: case 18: case 19: case 20: case 21: case 22: case 23: case 24: case 25:
+            return launch_config_bt<DT>(cfg, a, grid, s);   // the ring kernels take either B layout
         default: return hipErrorInvalidValue;
     }
 }

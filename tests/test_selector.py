@@ -57,7 +57,7 @@ def test_alignment_routes_to_generic(dtype):
     assert p["kernel"] == b.GEMM_KERNEL_GENERIC
     # everything aligned -> vectorised family
     p = plan(dtype, 512, 512, 4096)
-    assert p["kernel"] in (b.GEMM_KERNEL_MACRO, b.GEMM_KERNEL_SKINNY, b.GEMM_KERNEL_DIRECT)
+    assert p["kernel"] in (b.GEMM_KERNEL_MACRO, b.GEMM_KERNEL_SKINNY, b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING)
 
 
 @pytest.mark.parametrize("dtype", ["int8", "bf16"])
@@ -178,19 +178,19 @@ def plan_bt(dtype, M, N, K, ldbt=None, off=0):
 
 @pytest.mark.parametrize("dtype", [I8, BF])
 def test_column_major_b_plans(dtype):
-    """B stored N x K runs on the configurations built for it (the generic and direct
-    families), with the same tiling invariants; alignment of Bt rows is judged on K."""
+    """B stored N x K runs on the configurations built for it (the generic, direct and
+    ring families), with the same tiling invariants; alignment of Bt rows is judged on K."""
     for M, N, K in itertools.product([1, 17, 64, 257, 4096], [1, 8, 33, 256, 4000], [0, 1, 16, 100, 8192]):
         p = plan_bt(dtype, M, N, K)
         check_invariants(p, dtype, M, N, K)
-        assert p["kernel"] in (b.GEMM_KERNEL_GENERIC, b.GEMM_KERNEL_DIRECT)
+        assert p["kernel"] in (b.GEMM_KERNEL_GENERIC, b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING)
         assert not p["name"].startswith("pingpong")
     # N need not be a multiple of 16 bytes for column-major B, K must
-    assert plan_bt(dtype, 512, 4100, 4096)["kernel"] == b.GEMM_KERNEL_DIRECT
+    assert plan_bt(dtype, 512, 4100, 4096)["kernel"] in (b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING)
     assert plan_bt(dtype, 512, 512, 4097)["kernel"] == b.GEMM_KERNEL_GENERIC
     assert plan_bt(dtype, 512, 512, 4096, off=ESZ[dtype])["kernel"] == b.GEMM_KERNEL_GENERIC
     big = plan_bt(dtype, 8192, 8192, 8192)
-    assert big["kernel"] == b.GEMM_KERNEL_DIRECT and big["bm"] == 256 and big["bn"] == 256
+    assert big["kernel"] in (b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING) and big["bm"] == 256 and big["bn"] == 256
 
 
 def test_column_major_b_rejects_configs_without_it():
