@@ -79,7 +79,8 @@ typedef enum {
     GEMM_KERNEL_MACRO = 1,   /* 16-byte vector loads, large LDS macro-tiles    */
     GEMM_KERNEL_SKINNY = 2,  /* small M: narrow M tile, wide N, split-K        */
     GEMM_KERNEL_DIRECT = 3,  /* global -> LDS direct loads, LDS transpose reads */
-    GEMM_KERNEL_RING = 4     /* as DIRECT, 64-byte K slots in a deeper LDS ring */
+    GEMM_KERNEL_RING = 4,    /* as DIRECT, 64-byte K slots in a deeper LDS ring */
+    GEMM_KERNEL_GEMV = 5     /* M = 1: matrix-vector kernels on the vector ALUs */
 } gemm_kernel_t;
 
 /* The selector's choice for one call (filled by gemm_plan). */
@@ -88,7 +89,7 @@ typedef struct gemm_plan_info {
     int32_t config;          /* index of the tile configuration in the family  */
     int32_t bm, bn, bk;      /* workgroup macro-tile (bk in elements)          */
     int32_t waves;           /* wavefronts per workgroup                       */
-    int32_t mfma_m, mfma_n, mfma_k;  /* MFMA instruction shape                 */
+    int32_t mfma_m, mfma_n, mfma_k;  /* MFMA instruction shape (0: none, GEMV) */
     int32_t split_k;         /* K slices (1 = no split)                        */
     int32_t reduce_in_kernel;/* split-K partials summed by the last slice of each
                                 tile inside the GEMM kernel (1) or by a second

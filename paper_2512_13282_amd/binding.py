@@ -33,6 +33,7 @@ GEMM_KERNEL_MACRO = 1
 GEMM_KERNEL_SKINNY = 2
 GEMM_KERNEL_DIRECT = 3
 GEMM_KERNEL_RING = 4
+GEMM_KERNEL_GEMV = 5
 
 EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt", "gemm_plan",
             "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",

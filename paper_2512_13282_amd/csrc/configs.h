@@ -19,7 +19,8 @@ namespace gemm {
 
 enum Dtype : int32_t { DT_I8 = 0, DT_BF16 = 1 };
 
-enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2, FAM_DIRECT = 3, FAM_RING = 4 };
+enum Family : int32_t { FAM_GENERIC = 0, FAM_MACRO = 1, FAM_SKINNY = 2, FAM_DIRECT = 3, FAM_RING = 4,
+                        FAM_GEMV = 5 };
 
 struct TileConfig {
     int32_t family;
@@ -46,6 +47,9 @@ constexpr int32_t kSlotKBytes = 64;
 // Family MACRO: 16-byte vector loads staged through registers (B transposed
 // in registers); large tiles.
 // Family SKINNY: same loaders, narrow M tile for M <= 64.
+// Family GEMV: M = 1 only, vector-ALU matrix-vector kernels, one per B layout
+// (col_major_b = 1 marks the column-major-only one); the efficiencies are the
+// vector-ALU multiply-add rate as a fraction of the MFMA peak.
 // Family DIRECT: both operands stream global -> LDS directly (buffer loads with
 // an LDS destination); B's fragments come from LDS transpose reads, or, for B
 // stored column-major, from 16-byte reads like A's.
@@ -77,6 +81,8 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,      64, 128, 1, 4, 1, 8, 0.18, 0.20, 1, "ring_64x128_w4"},
     {FAM_RING,      32, 256, 1, 4, 1, 6, 0.15, 0.18, 1, "ring_32x256_w4"},
     {FAM_RING,      64, 256, 1, 4, 1, 6, 0.22, 0.26, 1, "ring_64x256_w4"},
+    {FAM_GEMV,       1, 1024, 1, 4, 4, 1, 0.03, 0.06, 0, "gemv_1024"},
+    {FAM_GEMV,       1,  16, 1, 4, 4, 1, 0.03, 0.06, 1, "gemv_bt_16"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 
@@ -84,6 +90,7 @@ constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 // B stage (bn x 128 B).  The analog of the paper's L1 budget (Eq. 5) without
 // the C term: the output tile lives in registers, not in LDS.
 constexpr int64_t lds_bytes(const TileConfig &c) {
+    if (c.family == FAM_GEMV) return c.col_major_b ? 4 * int64_t(c.bn) : 4 * 4 * int64_t(c.bn);
     return int64_t(c.stages) * (int64_t(c.bm) + int64_t(c.bn)) * (c.family == FAM_RING ? kSlotKBytes : kStageKBytes);
 }
 

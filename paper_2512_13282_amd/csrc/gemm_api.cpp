@@ -199,9 +199,10 @@ static int plan_impl(int dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K
     out->bn = c.bn;
     out->bk = gemm::stage_k_elems(dtype);
     out->waves = c.wm * c.wn;
-    out->mfma_m = 32;
-    out->mfma_n = 32;
-    out->mfma_k = dtype == GEMM_DTYPE_I8_I32 ? 32 : 16;
+    const bool mfma = c.family != gemm::FAM_GEMV;      // the matrix-vector kernels use the vector ALUs
+    out->mfma_m = mfma ? 32 : 0;
+    out->mfma_n = mfma ? 32 : 0;
+    out->mfma_k = mfma ? (dtype == GEMM_DTYPE_I8_I32 ? 32 : 16) : 0;
     out->split_k = pl.split_k;
     out->reduce_in_kernel = pl.split_k > 1 ? pl.reduce_in_kernel : 0;
     out->k_chunk = pl.k_chunk;
@@ -228,7 +229,7 @@ int gemm_plan_bt(int dtype, int64_t M, int64_t N, int64_t K, int64_t lda, int64_
 int gemm_force_plan(int dtype, int kernel, int config, int split_k) {
     if (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32) return GEMM_ERR_INVALID_VALUE;
     if (split_k < 0 || config < -1 || config >= gemm::kNumConfigs) return GEMM_ERR_INVALID_VALUE;
-    if (kernel < GEMM_KERNEL_AUTO || kernel > GEMM_KERNEL_RING) return GEMM_ERR_INVALID_VALUE;
+    if (kernel < GEMM_KERNEL_AUTO || kernel > GEMM_KERNEL_GEMV) return GEMM_ERR_INVALID_VALUE;
     if (config >= 0 && kernel >= 0 && gemm::kConfigs[config].family != kernel) return GEMM_ERR_INVALID_VALUE;
     std::lock_guard<std::mutex> lk(g_mu);
     Override &o = g_override[dtype];

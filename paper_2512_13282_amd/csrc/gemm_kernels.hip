@@ -1784,6 +1784,262 @@ void gemm_stream_kernel(KernelArgs args) {
     store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0, n0 + wcol0, lane);
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-vector kernels for M = 1 (the paper's stated future work: GEMV).  With
+// one row of A there is no reuse to stage through LDS or to feed MFMAs with: the
+// work is a single pass over B, bound by HBM bandwidth, so these kernels only
+// keep enough 16-byte loads in flight and do the few multiply-adds per byte on
+// the vector ALUs.
+//
+// Row-major B (gemv_kernel): a workgroup owns 1024 columns of one K slice; lane l
+// of each wave holds 16 consecutive columns (16 int8 or 2 x 8 bf16 per row), the
+// four waves take every fourth row of the slice, and their partial sums meet in
+// LDS at the end.
+//
+// Column-major B (gemv_bt_kernel, B stored N x K): a workgroup owns 16 columns
+// (rows of the stored matrix), four per wave; the lanes of a wave split K in
+// 16-byte pieces and accumulate with the 4-way int8 dot-product instruction
+// (bf16: widened to fp32, fused multiply-adds), then a butterfly over the wave
+// sums the lanes.
+//
+// Split-K uses the partial planes and arrival counters of the tile kernels,
+// with the same fixed slice order.
+// ---------------------------------------------------------------------------
+template <int DT>
+using gemv_acc_t = typename std::conditional<DT == DT_I8, int32_t, float>::type;
+template <int DT>
+using gemv_sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;   // int32 wraps mod 2^32
+
+// Writes `cols` results v[c] of columns n0 + c (one output row) for K slice
+// `slice`: straight into C without split-K, else into the slice's partial plane;
+// with the in-kernel reduction the workgroup arriving last for this column block
+// sums the planes in slice order.  Thread t handles c = t, t + 256, ...
+template <int DT, int COLS>
+__device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_acc_t<DT> *v, int64_t n0,
+                                           int tile, int slice) {
+    using out_t = typename Types<DT>::out_t;
+    using sum_t = gemv_sum_t<DT>;
+    const int64_t N = args.N;
+    out_t *C = static_cast<out_t *>(args.C);
+    sum_t *ws = static_cast<sum_t *>(args.workspace);
+    const int t = int(threadIdx.x);
+    if (args.split_k == 1) {
+        for (int c = t; c < COLS; c += 256)
+            if (n0 + c < N) C[n0 + c] = out_t(v[c]);
+        return;
+    }
+    if (!args.reduce_in_kernel) {
+        for (int c = t; c < COLS; c += 256)
+            if (n0 + c < N) ws[int64_t(slice) * N + n0 + c] = sum_t(v[c]);
+        return;
+    }
+    for (int c = t; c < COLS; c += 256)
+        if (n0 + c < N) store_coherent(&ws[int64_t(slice) * N + n0 + c], sum_t(v[c]));
+    __shared__ int s_last;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's partial stores are complete
+    __syncthreads();                                   // ... and every thread's
+    if (t == 0) {
+        const unsigned ticket = __hip_atomic_fetch_add(&args.counters[tile], 1u, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+        s_last = ticket == unsigned(args.split_k - 1);
+    }
+    __syncthreads();
+    if (!s_last) return;
+    // Sixteen slices per round trip: the loads of a batch are all issued before any is
+    // used, then added in slice order.
+    for (int c = t; c < COLS; c += 256) {
+        if (n0 + c >= N) continue;
+        sum_t s = sum_t(0);
+        for (int p0 = 0; p0 < args.split_k; p0 += 16) {
+            sum_t v16[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                v16[u] = load_coherent(&ws[int64_t(p0 + u < args.split_k ? p0 + u : 0) * N + n0 + c]);
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (p0 + u < args.split_k) s = (p0 + u == 0) ? v16[u] : s + v16[u];
+        }
+        C[n0 + c] = out_t(s);
+    }
+    if (t == 0) __hip_atomic_store(&args.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
+    using acc_t = gemv_acc_t<DT>;
+    constexpr int E = Types<DT>::E;
+    constexpr int CB = 1024;                   // columns per workgroup
+    constexpr int CPL = 16;                    // columns per lane
+    constexpr int PIECES = CPL * E / 16;       // 16-byte pieces per lane and row (1 int8, 2 bf16)
+    constexpr int U = 8 / PIECES;              // rows in flight per lane and iteration
+    const int lane = int(threadIdx.x) & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) >> 6);
+
+    int tm, tn, slice;
+    map_tile(args, tm, tn, slice);
+    (void)tm;
+    const int64_t N = args.N;
+    const int64_t n0 = int64_t(tn) * CB;
+    const int64_t col = n0 + int64_t(lane) * CPL;
+    const int64_t k_begin = int64_t(slice) * args.k_chunk;
+    int64_t k_end = k_begin + args.k_chunk;
+    if (k_end > args.K) k_end = args.K;
+    // N * E is a multiple of 16 bytes, so a 16-byte piece is either wholly inside a row or past its end.
+    bool piece_ok[PIECES];
+#pragma unroll
+    for (int h = 0; h < PIECES; ++h) piece_ok[h] = col + h * (16 / E) < N;
+
+    const uint8_t *const Ab = static_cast<const uint8_t *>(args.A);
+    const uint8_t *const Bb = static_cast<const uint8_t *>(args.B);
+    const int64_t ldb_b = args.ldb * E;
+
+    acc_t acc[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) acc[j] = acc_t(0);
+
+    // Batches of U rows (this wave's rows k0, k0 + 4, ..., k0 + 4(U-1)); the loads of
+    // the next batch are issued before the current one is consumed, so two batches
+    // are in flight per lane.
+    struct Batch {
+        u32x4_t v[U][PIECES];
+        acc_t a[U];
+    };
+    auto load_batch = [&](Batch &bt, int64_t k0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t k = k0 + 4 * u;
+            const bool row_ok = k < k_end;
+            const uint8_t *const row = Bb + k * ldb_b + col * E;
+#pragma unroll
+            for (int h = 0; h < PIECES; ++h)
+                bt.v[u][h] = (row_ok && piece_ok[h]) ? *reinterpret_cast<const u32x4_t *>(row + 16 * h)
+                                                     : u32x4_t{0u, 0u, 0u, 0u};
+            if constexpr (DT == DT_I8) {
+                bt.a[u] = row_ok ? acc_t(reinterpret_cast<const int8_t *>(Ab)[k]) : acc_t(0);
+            } else {
+                const uint32_t bits = row_ok ? uint32_t(reinterpret_cast<const uint16_t *>(Ab)[k]) : 0u;
+                bt.a[u] = __uint_as_float(bits << 16);
+            }
+        }
+    };
+    auto use_batch = [&](const Batch &bt) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int h = 0; h < PIECES; ++h)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const unsigned x = bt.v[u][h][w];
+                    if constexpr (DT == DT_I8) {
+#pragma unroll
+                        for (int b = 0; b < 4; ++b)
+                            acc[4 * w + b] += int32_t(int8_t(uint8_t(x >> (8 * b)))) * bt.a[u];
+                    } else {
+                        acc[8 * h + 2 * w] = fmaf(__uint_as_float(x << 16), bt.a[u], acc[8 * h + 2 * w]);
+                        acc[8 * h + 2 * w + 1] =
+                            fmaf(__uint_as_float(x & 0xffff0000u), bt.a[u], acc[8 * h + 2 * w + 1]);
+                    }
+                }
+    };
+    constexpr int64_t STEP = 4 * U;            // rows advanced per batch (four waves interleaved)
+    Batch b0, b1;
+    int64_t k0 = k_begin + wave;
+    if (k0 < k_end) load_batch(b0, k0);
+    for (; k0 < k_end; k0 += 2 * STEP) {
+        if (k0 + STEP < k_end) load_batch(b1, k0 + STEP);
+        use_batch(b0);
+        if (k0 + STEP >= k_end) break;
+        if (k0 + 2 * STEP < k_end) load_batch(b0, k0 + 2 * STEP);
+        use_batch(b1);
+    }
+
+    // The four waves' partial sums of the same columns, added in wave order.
+    __shared__ acc_t red[4][CB];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) red[wave][lane * CPL + j] = acc[j];
+    __syncthreads();
+    acc_t tot[CB / 256];
+#pragma unroll
+    for (int i = 0; i < CB / 256; ++i) {
+        const int c = int(threadIdx.x) + 256 * i;
+        tot[i] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < CB / 256; ++i) red[0][int(threadIdx.x) + 256 * i] = tot[i];
+    __syncthreads();
+    gemv_store<DT, CB>(args, red[0], n0, tn, slice);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void gemv_bt_kernel(KernelArgs args) {
+    using acc_t = gemv_acc_t<DT>;
+    constexpr int E = Types<DT>::E;
+    constexpr int VECE = 16 / E;               // K elements per 16-byte piece
+    constexpr int R = 4;                       // columns (stored rows) per wave
+    constexpr int CB = 4 * R;                  // columns per workgroup
+    const int lane = int(threadIdx.x) & 63;
+    const int wave = int(threadIdx.x) >> 6;
+
+    int tm, tn, slice;
+    map_tile(args, tm, tn, slice);
+    (void)tm;
+    const int64_t N = args.N;
+    const int64_t n0 = int64_t(tn) * CB;
+    const int64_t k_begin = int64_t(slice) * args.k_chunk;
+    int64_t k_end = k_begin + args.k_chunk;
+    if (k_end > args.K) k_end = args.K;
+    const uint8_t *const Ab = static_cast<const uint8_t *>(args.A);
+    const uint8_t *const Bb = static_cast<const uint8_t *>(args.B);
+    const int64_t ldb_b = args.ldb * E;
+    bool row_ok[R];
+    const uint8_t *brow[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t n = n0 + wave * R + r;
+        row_ok[r] = n < N;
+        brow[r] = Bb + (row_ok[r] ? n : 0) * ldb_b;
+    }
+
+    acc_t acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = acc_t(0);
+    // K * E is a multiple of 16 bytes and so are the slice bounds: a piece is wholly in or out.
+    for (int64_t k = k_begin + int64_t(lane) * VECE; k < k_end; k += 64 * VECE) {
+        const u32x4_t a = *reinterpret_cast<const u32x4_t *>(Ab + k * E);
+        u32x4_t b[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            b[r] = row_ok[r] ? *reinterpret_cast<const u32x4_t *>(brow[r] + k * E) : u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                if constexpr (DT == DT_I8) {
+                    acc[r] = __builtin_amdgcn_sdot4(int(a[w]), int(b[r][w]), acc[r], false);
+                } else {
+                    // Both bf16 halves widened exactly to fp32, then two fused multiply-adds.
+                    acc[r] = fmaf(__uint_as_float(a[w] << 16), __uint_as_float(b[r][w] << 16), acc[r]);
+                    acc[r] = fmaf(__uint_as_float(a[w] & 0xffff0000u), __uint_as_float(b[r][w] & 0xffff0000u), acc[r]);
+                }
+            }
+    }
+    // Butterfly over the 64 lanes: every lane ends with the wave's sums.
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) acc[r] += __shfl_xor(acc[r], m, 64);
+    __shared__ acc_t res[CB];
+    if (lane < R) {
+        acc_t v = acc[0];
+#pragma unroll
+        for (int r = 1; r < R; ++r) v = lane == r ? acc[r] : v;
+        res[wave * R + lane] = v;
+    }
+    __syncthreads();
+    gemv_store<DT, CB>(args, res, n0, tn, slice);
+}
+
 // Sums split-K partials [split][M][N] into C in slice order 0, 1, ... (the
 // same fixed order as the in-kernel reduction).
 template <typename T>
@@ -1864,6 +2120,9 @@ static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t gri
         case 23: return launch_ring<DT, 64, 128, 1, 4, 2, 8>(a, grid, s);
         case 24: return launch_ring<DT, 32, 256, 1, 4, 1, 6>(a, grid, s);
         case 25: return launch_ring<DT, 64, 256, 1, 4, 1, 6>(a, grid, s);
+        case 27:
+            hipLaunchKernelGGL((gemv_bt_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
+            return hipGetLastError();
         default: return hipErrorInvalidValue;
     }
 }
@@ -1896,6 +2155,9 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
             return hipGetLastError();
         case 16: case 17: case 18: case 19: case 20: case 21: case 22: case 23: case 24: case 25:
             return launch_config_bt<DT>(cfg, a, grid, s);   // the ring kernels take either B layout
+        case 26:
+            hipLaunchKernelGGL((gemv_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
+            return hipGetLastError();
         default: return hipErrorInvalidValue;
     }
 }

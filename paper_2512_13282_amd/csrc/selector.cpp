@@ -45,6 +45,7 @@ bool config_applicable(const Problem &p, int32_t cfg) {
     if (cfg < 0 || cfg >= kNumConfigs) return false;
     const TileConfig &c = kConfigs[cfg];
     if (p.trans_b && !c.col_major_b) return false;
+    if (c.family == FAM_GEMV) return p.M == 1 && (c.col_major_b != 0) == (p.trans_b != 0) && vector_loads_ok(p);
     if (c.family == FAM_GENERIC) return true;
     return vector_loads_ok(p);
 }
@@ -114,15 +115,16 @@ struct TunedPlan {
     int64_t M, N, K;
     int32_t config, split;
     int32_t reduce;      // -1: the model's choice
+    int32_t trans_b;     // B layout the plan was measured with (1: column-major)
 };
 static const TunedPlan kTuned[] = {
 #include "tuned_plans.inc"
-    {-1, 0, 0, 0, 0, 0, -1},   // sentinel
+    {-1, 0, 0, 0, 0, 0, -1, 0},   // sentinel
 };
 
 bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce) {
     for (const TunedPlan &t : kTuned) {
-        if (!p.trans_b && t.dtype == p.dtype && t.M == p.M && t.N == p.N && t.K == p.K &&
+        if (t.trans_b == p.trans_b && t.dtype == p.dtype && t.M == p.M && t.N == p.N && t.K == p.K &&
             t.config >= 0 && t.config < kNumConfigs && config_applicable(p, t.config)) {
             *config = t.config;
             *split = t.split;

@@ -123,7 +123,7 @@ def _tuned_entries():
                         "paper_2512_13282_amd", "csrc", "tuned_plans.inc")
     out = []
     for line in open(path):
-        m = re.match(r"\s*\{(-?\d+), (\d+), (\d+), (\d+), (\d+), (\d+), (-?\d+)\},", line)
+        m = re.match(r"\s*\{(-?\d+), (\d+), (\d+), (\d+), (\d+), (\d+), (-?\d+), ([01])\},", line)
         if m:
             out.append(tuple(int(x) for x in m.groups()))
     return out
@@ -134,8 +134,8 @@ def test_tuned_plans_are_valid_and_used():
     gemm_plan returns it (no override active, aligned operands)."""
     entries = _tuned_entries()
     assert entries, "tuned_plans.inc holds no plans"
-    for (d, M, N, K, cfg, split, reduce) in entries:
-        p = plan(d, M, N, K)
+    for (d, M, N, K, cfg, split, reduce, bt) in entries:
+        p = plan_bt(d, M, N, K) if bt else plan(d, M, N, K)
         assert p["config"] == cfg, (d, M, N, K, p["name"])
         if reduce >= 0 and p["split_k"] > 1:
             assert p["reduce_in_kernel"] == reduce
@@ -145,7 +145,7 @@ def test_tuned_plans_are_valid_and_used():
 
 def test_tuned_plans_skip_misaligned_operands():
     # the same shape with a misaligned A pointer falls back to the alignment-agnostic family
-    (d, M, N, K, cfg, split, reduce) = _tuned_entries()[0]
+    (d, M, N, K, cfg, split, reduce, bt) = _tuned_entries()[0]
     p = plan(d, M, N, K, off=ESZ[d])
     assert p["kernel"] == b.GEMM_KERNEL_GENERIC
 
@@ -183,8 +183,9 @@ def test_column_major_b_plans(dtype):
     for M, N, K in itertools.product([1, 17, 64, 257, 4096], [1, 8, 33, 256, 4000], [0, 1, 16, 100, 8192]):
         p = plan_bt(dtype, M, N, K)
         check_invariants(p, dtype, M, N, K)
-        assert p["kernel"] in (b.GEMM_KERNEL_GENERIC, b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING)
-        assert not p["name"].startswith("pingpong")
+        fams = (b.GEMM_KERNEL_GENERIC, b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING)
+        assert p["kernel"] in fams + ((b.GEMM_KERNEL_GEMV,) if M == 1 else ())
+        assert p["name"] != "gemv_1024" and not p["name"].startswith("pingpong")
     # N need not be a multiple of 16 bytes for column-major B, K must
     assert plan_bt(dtype, 512, 4100, 4096)["kernel"] in (b.GEMM_KERNEL_DIRECT, b.GEMM_KERNEL_RING)
     assert plan_bt(dtype, 512, 512, 4097)["kernel"] == b.GEMM_KERNEL_GENERIC
@@ -203,3 +204,31 @@ def test_column_major_b_rejects_configs_without_it():
             plan(I8, 512, 512, 4096)      # the row-major form still runs it
     finally:
         b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
+
+
+GEMV_RM, GEMV_BT = 26, 27
+
+
+@pytest.mark.parametrize("dtype", [I8, BF])
+def test_gemv_configs_only_for_one_row(dtype):
+    """The matrix-vector kernels run M = 1 only, each with its own B layout."""
+    try:
+        b.gemm_force_plan(dtype, b.GEMM_KERNEL_AUTO, GEMV_RM, 0)
+        p = plan(dtype, 1, 14336, 4096)
+        assert p["name"] == "gemv_1024" and p["kernel"] == b.GEMM_KERNEL_GEMV
+        assert p["mfma_m"] == p["mfma_n"] == p["mfma_k"] == 0 and p["bm"] == 1
+        check_invariants(p, dtype, 1, 14336, 4096)
+        for M in (2, 16):
+            with pytest.raises(b.GemmError) as e:
+                plan(dtype, M, 14336, 4096)
+            assert e.value.status == b.GEMM_ERR_UNSUPPORTED
+        with pytest.raises(b.GemmError):
+            plan_bt(dtype, 1, 14336, 4096)                  # row-major-B kernel only
+        b.gemm_force_plan(dtype, b.GEMM_KERNEL_AUTO, GEMV_BT, 0)
+        p = plan_bt(dtype, 1, 4096, 14336)
+        assert p["name"] == "gemv_bt_16" and p["bn"] == 16
+        check_invariants(p, dtype, 1, 4096, 14336)
+        with pytest.raises(b.GemmError):
+            plan(dtype, 1, 4096, 14336)                     # column-major-B kernel only
+    finally:
+        b.gemm_force_plan(dtype, b.GEMM_KERNEL_AUTO, -1, 0)
