@@ -276,12 +276,13 @@ def write_traffic(fetch_csv: str, write_csv: str) -> None:
     S = 8192
     workloads = {}
     for k in fetch:
-        # gemm_lds_kernel<dtype, BM, BN, WM, WN, waves/EU, B column-major>: one plan per workload
-        if "gemm::gemm_lds_kernel<" not in k:
+        # gemm_lds_kernel<dtype, BM, BN, WM, WN, waves/EU, B column-major> and
+        # gemm_ring_kernel<..., B column-major, ring depth>: one plan per workload
+        if "gemm::gemm_lds_kernel<" not in k and "gemm::gemm_ring_kernel<" not in k:
             continue
         targs = [t.strip() for t in k.split("<", 1)[1].split(">", 1)[0].split(",")]
         dtype = "int8" if targs[0] == "0" else "bf16"
-        bt = targs[-1] == "true"
+        bt = targs[6] == "true"
         e = 1 if dtype == "int8" else 2
         comp = S * S * e * 2 + S * S * 4
         fb = fetch[k] * 1024.0 * f_scale
