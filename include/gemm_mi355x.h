@@ -101,7 +101,7 @@ typedef struct gemm_plan_info {
     double  model_traffic_bytes; /* modelled global traffic: A and B re-reads
                                     (A ~ MNK/BN, B ~ MNK/BM), C, partials      */
     double  model_t_comp_us; /* modelled MFMA time at the plan's efficiency    */
-    double  model_t_mem_us;  /* modelled memory time at 8 TB/s                 */
+    double  model_t_mem_us;  /* modelled memory time (sustained HBM rate, L2 re-reads) */
     char    name[48];        /* human-readable kernel/config name              */
 } gemm_plan_info;
 
