@@ -14,6 +14,11 @@ row-major layouts of Sec. 4.2.2 (Memory Tile Design):
 
 Every function takes numpy arrays (2-D, row stride free, unit column stride).
 
+``requant_i32`` and ``round_bf16`` turn exact results into the reduced output
+precisions the paper also reports (int8 -> int8 / int16, bf16 -> bf16; Sec. 5.1,
+Sec. 5.2.3), by the rounding rules stated in ``oracle_gemm.c`` (the paper gives
+none).
+
 The ``*_bt`` forms take B stored column-major, i.e. as its transpose Bt (N x K),
 the layout the paper prefers for B (Sec. 4.3).  They form B = Bt^T with a plain
 transposing copy and call the row-major routine: the same products summed in
@@ -37,7 +42,7 @@ CFLAGS = ["-O2", "-fPIC", "-shared", "-pthread", "-std=c11", "-fno-fast-math"]
 
 def build(src: str = SRC, out: str = LIB, extra_flags: list[str] | None = None) -> str:
     """Compile the oracle with gcc into ``out`` (always recompiles)."""
-    cmd = ["gcc", *CFLAGS, *(extra_flags or []), src, "-o", out + ".tmp"]
+    cmd = ["gcc", *CFLAGS, *(extra_flags or []), src, "-o", out + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(out + ".tmp", out)
     return out
@@ -64,6 +69,12 @@ class Oracle:
         lib.oracle_freivalds_i8_i32.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64,
                                                 ctypes.c_int, ctypes.c_uint64]
         lib.oracle_freivalds_i8_i32.restype = i64
+        lib.oracle_requant_i32.argtypes = [p, i64, ctypes.c_int, ctypes.c_int, p]
+        lib.oracle_requant_i32.restype = ctypes.c_int
+        lib.oracle_round_bf16.argtypes = [p, i64, p]
+        lib.oracle_round_bf16.restype = ctypes.c_int
+        lib.oracle_bf16_from_double.argtypes = [ctypes.c_double]
+        lib.oracle_bf16_from_double.restype = ctypes.c_uint16
         self.lib = lib
 
     # -- helpers -----------------------------------------------------------
@@ -164,6 +175,30 @@ class Oracle:
         if bad < 0:
             raise RuntimeError(f"oracle_freivalds_i8_i32 failed ({bad})")
         return int(bad)
+
+
+    # -- reduced-precision outputs ---------------------------------------------
+    def requant_i32(self, C: np.ndarray, shift: int, bits: int) -> np.ndarray:
+        """int32 results -> int8 (bits 8) or int16 (bits 16): C / 2^shift rounded to
+        nearest, ties to even, then saturated."""
+        src = np.ascontiguousarray(C, dtype=np.int32)
+        out = np.empty(src.shape, dtype=np.int32)
+        rc = self.lib.oracle_requant_i32(src.ctypes.data, src.size, int(shift), int(bits), out.ctypes.data)
+        if rc != 0:
+            raise RuntimeError(f"oracle_requant_i32 failed ({rc})")
+        return out.astype(np.int8 if bits == 8 else np.int16)
+
+    def round_bf16(self, C: np.ndarray) -> np.ndarray:
+        """fp64 values -> nearest bf16 (ties to even), as uint16 bit patterns."""
+        src = np.ascontiguousarray(C, dtype=np.float64)
+        out = np.empty(src.shape, dtype=np.uint16)
+        rc = self.lib.oracle_round_bf16(src.ctypes.data, src.size, out.ctypes.data)
+        if rc != 0:
+            raise RuntimeError(f"oracle_round_bf16 failed ({rc})")
+        return out
+
+    def bf16_from_double(self, x: float) -> int:
+        return int(self.lib.oracle_bf16_from_double(float(x)))
 
 
 _default: Oracle | None = None

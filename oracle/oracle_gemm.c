@@ -31,6 +31,7 @@
  *
  * Strides: lda, ldb, ldc are row strides in elements (row-major storage).
  */
+#include <math.h>
 #include <pthread.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -256,4 +257,73 @@ int64_t oracle_freivalds_i8_i32(int64_t M, int64_t N, int64_t K,
     free(r);
     free(br);
     return bad;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Reduced-precision outputs.  The paper also reports int8 GEMMs with int16  */
+/* and int8 outputs ("precision-reduced") and bf16 GEMMs with bf16 outputs  */
+/* (Sec. 5.1, Sec. 5.2.3) but states no rounding or requantisation rule.    */
+/* The reading implemented here, applied elementwise to the exact results   */
+/* of the routines above:                                                   */
+/*                                                                          */
+/*   int32 -> int8 / int16 : q = v / 2^shift rounded to the nearest integer, */
+/*                            ties to even, then clamped to the output range; */
+/*   fp64  -> bf16         : the nearest bf16 value, ties to even (8          */
+/*                            significant bits, subnormal spacing 2^-133,     */
+/*                            values beyond the largest finite bf16 after      */
+/*                            rounding become infinities).                     */
+/* ------------------------------------------------------------------------ */
+
+/* Nearest integer to v / 2^shift, ties to even, computed exactly in int64. */
+static int64_t div_pow2_nearest_even(int64_t v, int shift)
+{
+    const int64_t d = (int64_t)1 << shift;
+    int64_t q = v / d;                       /* truncates toward zero */
+    if (v % d != 0 && v < 0) q -= 1;         /* floor */
+    const int64_t r = v - q * d;             /* 0 <= r < d */
+    if (shift > 0) {
+        const int64_t half = d / 2;
+        if (r > half || (r == half && q % 2 != 0)) q += 1;
+    }
+    return q;
+}
+
+int oracle_requant_i32(const int32_t *in, int64_t n, int shift, int bits, int32_t *out)
+{
+    if (n < 0 || (n > 0 && (in == NULL || out == NULL)) || shift < 0 || shift > 31 ||
+        (bits != 8 && bits != 16))
+        return ORACLE_EINVAL;
+    const int64_t hi = ((int64_t)1 << (bits - 1)) - 1, lo = -hi - 1;
+    for (int64_t i = 0; i < n; ++i) {
+        int64_t q = div_pow2_nearest_even((int64_t)in[i], shift);
+        if (q > hi) q = hi;
+        if (q < lo) q = lo;
+        out[i] = (int32_t)q;
+    }
+    return ORACLE_OK;
+}
+
+uint16_t oracle_bf16_from_double(double x)
+{
+    const uint16_t sign = signbit(x) ? 0x8000u : 0u;
+    const double ax = fabs(x);
+    if (ax == 0.0) return sign;
+    int e;
+    (void)frexp(ax, &e);                     /* ax = m * 2^e, 0.5 <= m < 1 */
+    int ulp_exp = e - 8;                     /* 8 significant bits */
+    if (ulp_exp < -133) ulp_exp = -133;      /* subnormal bf16 spacing */
+    const double r = nearbyint(ldexp(ax, -ulp_exp));   /* ties to even (default mode) */
+    const double y = ldexp(r, ulp_exp);
+    if (y > 0x1.fep127) return (uint16_t)(sign | 0x7F80u);   /* beyond the largest finite bf16 */
+    const float f = (float)y;                /* exact: y has at most 8 significant bits */
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return (uint16_t)(sign | (uint16_t)((u >> 16) & 0x7FFFu));
+}
+
+int oracle_round_bf16(const double *in, int64_t n, uint16_t *out)
+{
+    if (n < 0 || (n > 0 && (in == NULL || out == NULL))) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_bf16_from_double(in[i]);
+    return ORACLE_OK;
 }

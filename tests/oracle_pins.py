@@ -339,4 +339,104 @@ def pin_bf16_bt_exact_rational_tiny(o):
                 assert abs(Fraction(float(C[i, j])) - exact) <= bound, (M, N, K, i, j)
 
 
+# ----------------------------------------------------------------------------- reduced-precision outputs
+def _i32_values(s: int, rng) -> list[int]:
+    """int32 values around the rounding and saturation boundaries of shift s."""
+    d = 2 ** s
+    cand = [0, 1, -1, 2, -2, 127, 128, -128, -129, 32767, 32768, -32768, -32769, 2 ** 31 - 1, -2 ** 31]
+    for m in range(-5, 6):
+        for off in (-1, 0, 1):
+            cand += [m * d + d // 2 + off, m * d + off, 127 * d + off, -128 * d + off,
+                     32767 * d + d // 2 + off, -32768 * d - d // 2 + off]
+    cand += [int(x) for x in rng.integers(-2 ** 31, 2 ** 31, size=200)]
+    return [v for v in cand if -2 ** 31 <= v < 2 ** 31]
+
+
+def pin_requant_exact_rational(o):
+    """int32 -> int8 / int16 for every shift 0..31 against exact rational rounding to the
+    nearest integer, ties to even (Python's round of a Fraction), then saturation."""
+    rng = RNG(31)
+    for s in range(32):
+        vals = _i32_values(s, rng)
+        arr = np.array(vals, dtype=np.int32)
+        for bits in (8, 16):
+            lo, hi = -(2 ** (bits - 1)), 2 ** (bits - 1) - 1
+            got = o.requant_i32(arr, s, bits)
+            assert got.dtype == (np.int8 if bits == 8 else np.int16)
+            for v, g in zip(vals, got.tolist()):
+                ref = min(hi, max(lo, round(Fraction(v, 2 ** s))))
+                assert g == ref, (v, s, bits, g, ref)
+
+
+def pin_requant_closed_forms(o):
+    """Hand-checked cases: halves go to the even neighbour, both signs; saturation at both ends."""
+    cases = [  # (value, shift, bits, expected)
+        (1, 1, 8, 0), (3, 1, 8, 2), (5, 1, 8, 2), (7, 1, 8, 4), (-1, 1, 8, 0), (-3, 1, 8, -2),
+        (-5, 1, 8, -2), (6, 2, 8, 2), (10, 2, 8, 2), (14, 2, 8, 4), (-6, 2, 8, -2), (9, 2, 8, 2),
+        (255, 1, 8, 127), (-257, 1, 8, -128), (256, 1, 8, 127), (-256, 1, 8, -128), (-255, 1, 8, -128),
+        (2 ** 31 - 1, 0, 16, 32767), (-2 ** 31, 0, 16, -32768), (-2 ** 31, 31, 8, -1),
+        (2 ** 31 - 1, 31, 8, 1), (2 ** 30, 31, 8, 0), (3 * 2 ** 29, 31, 8, 1), (234881024, 20, 8, 127),
+        (234881024, 20, 16, 224), (-234881024, 22, 16, -56), (100, 0, 8, 100), (-100, 0, 16, -100),
+    ]
+    for v, s, bits, want in cases:
+        got = int(o.requant_i32(np.array([v], dtype=np.int32), s, bits)[0])
+        assert got == want, (v, s, bits, got, want)
+
+
+def _bf16_rne_from_f32_bits(f: np.ndarray) -> np.ndarray:
+    """Round finite binary32 values to bf16, ties to even, on their bit patterns."""
+    u = f.astype(np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def pin_bf16_round_fp32_values(o):
+    """For values that are binary32 numbers, rounding the double equals rounding the binary32
+    bit pattern (an independent formulation), across normal and subnormal magnitudes."""
+    rng = RNG(32)
+    f = np.concatenate([
+        rng.standard_normal(4000).astype(np.float32) * np.float32(1000),
+        (rng.standard_normal(1000) * 2.0 ** rng.integers(-140, 120, size=1000)).astype(np.float32),
+        np.array([1.0, -1.0, 3.0, 0.1, 1e30, -1e-40, 1e-45], dtype=np.float32),
+    ])
+    f = f[np.isfinite(f)]
+    got = o.round_bf16(f.astype(np.float64))
+    assert np.array_equal(got, _bf16_rne_from_f32_bits(f))
+
+
+def pin_bf16_round_exact_rational(o):
+    """Doubles that are not binary32 numbers (sums of bf16 products) against exact rational
+    rounding to 8 significant bits, ties to even."""
+    rng = RNG(33)
+    xs = list(rng.standard_normal(2000) * 300.0) + [1 + 2 ** -8 + 2 ** -40, 1 + 2 ** -8 - 2 ** -40,
+                                                     -(3 + 2 ** -6 + 2 ** -50), 2 ** -130 * 1.75]
+    for x in xs:
+        bits = o.bf16_from_double(float(x))
+        fr = Fraction(float(x))
+        sign = -1 if fr < 0 else 1
+        a = abs(fr)
+        e = a.numerator.bit_length() - a.denominator.bit_length()
+        if Fraction(2) ** e > a:
+            e -= 1
+        ulp = Fraction(2) ** max(e - 7, -133)
+        ref = sign * round(a / ulp) * ulp
+        got = Fraction(o.bf16_to_double(bits))
+        assert got == ref, (x, hex(bits), float(ref))
+
+
+def pin_bf16_round_specials(o):
+    """Ties, signed zero, the largest finite value, overflow, and the subnormal range."""
+    cases = [
+        (1.0, 0x3F80), (1 + 2 ** -8, 0x3F80), (1 + 3 * 2 ** -8, 0x3F82), (-(1 + 2 ** -8), 0xBF80),
+        (1 + 2 ** -7, 0x3F81), (2 - 2 ** -8, 0x4000), (0.0, 0x0000), (-0.0, 0x8000),
+        (float.fromhex("0x1.fcp127"), 0x7F7E), (float.fromhex("0x1.fep127"), 0x7F7F),
+        (float.fromhex("0x1.fefffp127"), 0x7F7F), (float.fromhex("0x1.ffp127"), 0x7F80),
+        (-float.fromhex("0x1.ffp127"), 0xFF80), (float.fromhex("0x1.fdp127"), 0x7F7E),
+        (2.0 ** -133, 0x0001), (2.0 ** -134, 0x0000), (3 * 2.0 ** -134, 0x0002),
+        (2.0 ** -126, 0x0080), (-(2.0 ** -133), 0x8001),
+    ]
+    for x, want in cases:
+        got = o.bf16_from_double(x)
+        assert got == want, (x, hex(got), hex(want))
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

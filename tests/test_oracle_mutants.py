@@ -60,6 +60,30 @@ MUTANTS = [
     ("thread_rows_off_by_one",
      "j->row1 = M * (t + 1) / nthreads;",
      "j->row1 = M * (t + 1) / nthreads - (t + 1 < nthreads && M * (t + 1) / nthreads > M * t / nthreads ? 1 : 0);"),
+    ("requant_ties_away",
+     "if (r > half || (r == half && q % 2 != 0)) q += 1;",
+     "if (r >= half) q += 1;"),
+    ("requant_truncates",
+     "    if (shift > 0) {\n        const int64_t half",
+     "    if (shift < 0) {\n        const int64_t half"),
+    ("requant_no_floor",
+     "if (v % d != 0 && v < 0) q -= 1;",
+     "if (v % d != 0 && v > 0) q -= 0;"),
+    ("requant_clamp_low_off_by_one",
+     "hi = ((int64_t)1 << (bits - 1)) - 1, lo = -hi - 1;",
+     "hi = ((int64_t)1 << (bits - 1)) - 1, lo = -hi;"),
+    ("bf16_round_truncates",
+     "const double r = nearbyint(ldexp(ax, -ulp_exp));",
+     "const double r = trunc(ldexp(ax, -ulp_exp));"),
+    ("bf16_round_nine_bits",
+     "int ulp_exp = e - 8;",
+     "int ulp_exp = e - 9;"),
+    ("bf16_round_overflow_early",
+     "if (y > 0x1.fep127)",
+     "if (y > 0x1.fcp127)"),
+    ("bf16_round_no_subnormal_floor",
+     "if (ulp_exp < -133) ulp_exp = -133;",
+     "if (ulp_exp < -149) ulp_exp = -149;"),
     ("freivalds_skip_last_row",
      "for (int64_t i = 0; i < M; ++i) {\n            __int128 lhs",
      "for (int64_t i = 0; i < M - 1; ++i) {\n            __int128 lhs"),
