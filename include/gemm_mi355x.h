@@ -143,6 +143,47 @@ int gemm_bf16_f32_bt(int64_t M, int64_t N, int64_t K,
                      const uint16_t *Bt, int64_t ldbt,
                      float *C, int64_t ldc, void *stream);
 
+/* ---- Reduced-precision outputs ---------------------------------------------
+ * The same GEMMs with the output narrowed, the precisions the paper also
+ * reports (int8 -> int16 and int8 -> int8, and bf16 -> bf16; Sec. 5.1 and
+ * Sec. 5.2.3), which states no rounding or requantisation rule.  The rules here:
+ *
+ *   gemm_i8_i8 / gemm_i8_i16 : the exact int32 result (wrapping as gemm_i8_i32
+ *       documents) divided by 2^shift, rounded to the nearest integer with ties
+ *       to even, then saturated to [-128, 127] / [-32768, 32767]; 0 <= shift <= 31.
+ *   gemm_bf16_bf16 : the fp32 result of gemm_bf16_f32 rounded to the nearest
+ *       bf16, ties to even (raw bf16 bit patterns in C).
+ *
+ * C is int8_t / int16_t / uint16_t with row stride ldc in ELEMENTS of that type
+ * and must be aligned to its element size.  Plans, ownership, workspace,
+ * execution and errors are those of the int32 / fp32 calls (the plan does not
+ * depend on the output type); a shift outside [0, 31] is GEMM_ERR_INVALID_VALUE.
+ * The *_bt forms take B stored column-major (Bt, N x K) as above. */
+int gemm_i8_i8(int64_t M, int64_t N, int64_t K,
+               const int8_t *A, int64_t lda,
+               const int8_t *B, int64_t ldb,
+               int8_t *C, int64_t ldc, int shift, void *stream);
+int gemm_i8_i16(int64_t M, int64_t N, int64_t K,
+                const int8_t *A, int64_t lda,
+                const int8_t *B, int64_t ldb,
+                int16_t *C, int64_t ldc, int shift, void *stream);
+int gemm_bf16_bf16(int64_t M, int64_t N, int64_t K,
+                   const uint16_t *A, int64_t lda,
+                   const uint16_t *B, int64_t ldb,
+                   uint16_t *C, int64_t ldc, void *stream);
+int gemm_i8_i8_bt(int64_t M, int64_t N, int64_t K,
+                  const int8_t *A, int64_t lda,
+                  const int8_t *Bt, int64_t ldbt,
+                  int8_t *C, int64_t ldc, int shift, void *stream);
+int gemm_i8_i16_bt(int64_t M, int64_t N, int64_t K,
+                   const int8_t *A, int64_t lda,
+                   const int8_t *Bt, int64_t ldbt,
+                   int16_t *C, int64_t ldc, int shift, void *stream);
+int gemm_bf16_bf16_bt(int64_t M, int64_t N, int64_t K,
+                      const uint16_t *A, int64_t lda,
+                      const uint16_t *Bt, int64_t ldbt,
+                      uint16_t *C, int64_t ldc, void *stream);
+
 /* Pure host: the plan a GEMM call with these arguments would use (alignment
  * is taken from the three addresses, which are never dereferenced).
  * Returns GEMM_OK, GEMM_ERR_INVALID_VALUE or GEMM_ERR_UNSUPPORTED. */

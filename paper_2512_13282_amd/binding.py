@@ -1,7 +1,9 @@
 """Thin ctypes binding over libgemm_mi355x.so (argument marshalling only).
 
 The functions named like the C entry points (``gemm_i8_i32``, ``gemm_bf16_f32``,
-their column-major-B forms ``gemm_i8_i32_bt`` and ``gemm_bf16_f32_bt``, ``gemm_plan``,
+their column-major-B forms ``gemm_i8_i32_bt`` and ``gemm_bf16_f32_bt``, the
+reduced-precision-output forms ``gemm_i8_i8``, ``gemm_i8_i16``, ``gemm_bf16_bf16``
+and their ``*_bt`` forms, ``gemm_plan``,
 ``gemm_plan_bt``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
 ``gemm_status_string``, ``gemm_version``, and the measurement aid ``gemm_probe_mfma``)
 take plain integers and device addresses exactly as the C ABI does.  The two
@@ -35,7 +37,9 @@ GEMM_KERNEL_DIRECT = 3
 GEMM_KERNEL_RING = 4
 GEMM_KERNEL_GEMV = 5
 
-EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt", "gemm_plan",
+EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt",
+            "gemm_i8_i8", "gemm_i8_i16", "gemm_bf16_bf16", "gemm_i8_i8_bt", "gemm_i8_i16_bt",
+            "gemm_bf16_bf16_bt", "gemm_plan",
             "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",
             "gemm_status_string", "gemm_version", "gemm_probe_mfma")
 
@@ -87,6 +91,13 @@ def lib() -> ctypes.CDLL:
         l.gemm_i8_i32_bt.restype = i32
         l.gemm_bf16_f32_bt.argtypes = gemm_args
         l.gemm_bf16_f32_bt.restype = i32
+        shift_args = [i64, i64, i64, p, i64, p, i64, p, i64, i32, p]
+        for name in ("gemm_i8_i8", "gemm_i8_i16", "gemm_i8_i8_bt", "gemm_i8_i16_bt"):
+            getattr(l, name).argtypes = shift_args
+            getattr(l, name).restype = i32
+        for name in ("gemm_bf16_bf16", "gemm_bf16_bf16_bt"):
+            getattr(l, name).argtypes = gemm_args
+            getattr(l, name).restype = i32
         plan_args = [i32, i64, i64, i64, i64, i64, i64, ctypes.c_size_t, ctypes.c_size_t,
                      ctypes.c_size_t, ctypes.POINTER(PlanInfo)]
         l.gemm_plan.argtypes = plan_args
@@ -124,6 +135,31 @@ def gemm_i8_i32_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, stream=0) -> int:
 
 def gemm_bf16_f32_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, stream=0) -> int:
     return lib().gemm_bf16_f32_bt(M, N, K, A or None, lda, Bt or None, ldbt, C or None, ldc, stream or None)
+
+
+def gemm_i8_i8(M, N, K, A, lda, B, ldb, C, ldc, shift, stream=0) -> int:
+    return lib().gemm_i8_i8(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, shift, stream or None)
+
+
+def gemm_i8_i16(M, N, K, A, lda, B, ldb, C, ldc, shift, stream=0) -> int:
+    return lib().gemm_i8_i16(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, shift, stream or None)
+
+
+def gemm_bf16_bf16(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
+    return lib().gemm_bf16_bf16(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, stream or None)
+
+
+def gemm_i8_i8_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, shift, stream=0) -> int:
+    return lib().gemm_i8_i8_bt(M, N, K, A or None, lda, Bt or None, ldbt, C or None, ldc, shift, stream or None)
+
+
+def gemm_i8_i16_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, shift, stream=0) -> int:
+    return lib().gemm_i8_i16_bt(M, N, K, A or None, lda, Bt or None, ldbt, C or None, ldc, shift,
+                                stream or None)
+
+
+def gemm_bf16_bf16_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, stream=0) -> int:
+    return lib().gemm_bf16_bf16_bt(M, N, K, A or None, lda, Bt or None, ldbt, C or None, ldc, stream or None)
 
 
 def gemm_plan(dtype, M, N, K, lda, ldb, ldc, a_addr=0, b_addr=0, c_addr=0, trans_b=False) -> dict:

@@ -60,7 +60,9 @@ uint64_t span_bytes(int64_t rows, int64_t cols, int64_t ld, int64_t esize) {
     return uint64_t((rows - 1) * ld + cols) * uint64_t(esize);
 }
 
-int validate(const Problem &p, const void *A, const void *B, const void *C) {
+// c_esize: bytes per element of C (4 for the int32 / fp32 outputs, 1 or 2 for the
+// reduced-precision ones).
+int validate(const Problem &p, const void *A, const void *B, const void *C, int64_t c_esize = 4) {
     if (p.M < 0 || p.N < 0 || p.K < 0) return GEMM_ERR_INVALID_VALUE;
     const int64_t e = gemm::elem_bytes(p.dtype);
     const bool has_a = p.M > 0 && p.K > 0, has_b = p.K > 0 && p.N > 0, has_c = p.M > 0 && p.N > 0;
@@ -72,13 +74,13 @@ int validate(const Problem &p, const void *A, const void *B, const void *C) {
     // Natural alignment of the element types (a misaligned int32*/float*/bf16* is not a valid pointer).
     if (has_a && (uintptr_t(A) % uintptr_t(e)) != 0) return GEMM_ERR_INVALID_VALUE;
     if (has_b && (uintptr_t(B) % uintptr_t(e)) != 0) return GEMM_ERR_INVALID_VALUE;
-    if (has_c && (uintptr_t(C) % 4) != 0) return GEMM_ERR_INVALID_VALUE;
+    if (has_c && (uintptr_t(C) % uintptr_t(c_esize)) != 0) return GEMM_ERR_INVALID_VALUE;
     // Stride products must not overflow 64-bit byte offsets.
     const int64_t lim = int64_t(1) << 55;
     if (p.M > lim || p.N > lim || p.K > lim || (has_a && p.lda > lim / (p.M > 0 ? p.M : 1)) ||
         (has_b && p.ldb > lim / (b_rows > 0 ? b_rows : 1)) || (has_c && p.ldc > lim / (p.M > 0 ? p.M : 1)))
         return GEMM_ERR_INVALID_VALUE;
-    const uint64_t clen = span_bytes(p.M, p.N, p.ldc, 4);
+    const uint64_t clen = span_bytes(p.M, p.N, p.ldc, c_esize);
     if (has_c && has_a && overlaps(uintptr_t(C), clen, uintptr_t(A), span_bytes(p.M, p.K, p.lda, e)))
         return GEMM_ERR_INVALID_VALUE;
     if (has_c && has_b && overlaps(uintptr_t(C), clen, uintptr_t(B), span_bytes(b_rows, b_cols, p.ldb, e)))
@@ -116,9 +118,12 @@ int plan_for(const Problem &p, Plan *out) {
 }
 
 int run(int32_t dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
-        const void *B, int64_t ldb, void *C, int64_t ldc, void *stream) {
+        const void *B, int64_t ldb, void *C, int64_t ldc, void *stream,
+        int32_t epilogue = gemm::EPI_NONE, int32_t shift = 0) {
     Problem p{dtype, M, N, K, lda, ldb, ldc, uintptr_t(A), uintptr_t(B), uintptr_t(C), trans_b};
-    int rc = validate(p, A, B, C);
+    const int64_t c_esize = epilogue == gemm::EPI_I8 ? 1 : (epilogue == gemm::EPI_NONE ? 4 : 2);
+    if (shift < 0 || shift > 31) return GEMM_ERR_INVALID_VALUE;
+    int rc = validate(p, A, B, C, c_esize);
     if (rc != GEMM_OK) return rc;
     if (M == 0 || N == 0) return GEMM_OK;
     Plan pl;
@@ -142,6 +147,8 @@ int run(int32_t dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, const v
     a.group_m = 4;
     a.reduce_in_kernel = pl.reduce_in_kernel;
     a.b_trans = trans_b;
+    a.epilogue = epilogue;
+    a.shift = shift;
     if (pl.grid > 0x7fffffff || pl.tiles_m > 0x7fffffff || pl.tiles_n > 0x7fffffff)
         return GEMM_ERR_UNSUPPORTED;
     const int lr = gemm::launch_gemm(a, pl.config, pl.grid, stream);
@@ -172,6 +179,36 @@ int gemm_i8_i32_bt(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda
 int gemm_bf16_f32_bt(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *Bt,
                      int64_t ldbt, float *C, int64_t ldc, void *stream) {
     return run(gemm::DT_BF16, 1, M, N, K, A, lda, Bt, ldbt, C, ldc, stream);
+}
+
+int gemm_i8_i8(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *B,
+               int64_t ldb, int8_t *C, int64_t ldc, int shift, void *stream) {
+    return run(gemm::DT_I8, 0, M, N, K, A, lda, B, ldb, C, ldc, stream, gemm::EPI_I8, shift);
+}
+
+int gemm_i8_i16(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *B,
+                int64_t ldb, int16_t *C, int64_t ldc, int shift, void *stream) {
+    return run(gemm::DT_I8, 0, M, N, K, A, lda, B, ldb, C, ldc, stream, gemm::EPI_I16, shift);
+}
+
+int gemm_bf16_bf16(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *B,
+                   int64_t ldb, uint16_t *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_BF16, 0, M, N, K, A, lda, B, ldb, C, ldc, stream, gemm::EPI_BF16, 0);
+}
+
+int gemm_i8_i8_bt(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *Bt,
+                  int64_t ldbt, int8_t *C, int64_t ldc, int shift, void *stream) {
+    return run(gemm::DT_I8, 1, M, N, K, A, lda, Bt, ldbt, C, ldc, stream, gemm::EPI_I8, shift);
+}
+
+int gemm_i8_i16_bt(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *Bt,
+                   int64_t ldbt, int16_t *C, int64_t ldc, int shift, void *stream) {
+    return run(gemm::DT_I8, 1, M, N, K, A, lda, Bt, ldbt, C, ldc, stream, gemm::EPI_I16, shift);
+}
+
+int gemm_bf16_bf16_bt(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *Bt,
+                      int64_t ldbt, uint16_t *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_BF16, 1, M, N, K, A, lda, Bt, ldbt, C, ldc, stream, gemm::EPI_BF16, 0);
 }
 
 static int plan_impl(int dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb,

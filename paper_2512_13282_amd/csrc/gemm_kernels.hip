@@ -134,6 +134,41 @@ __device__ __forceinline__ T load_coherent(const T *p) {
     return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Output element idx (row * ldc + col, in output elements) of C from a result v of
+// the accumulator type, converted as the call's epilogue asks (launch.h).  int32
+// partial sums arrive as uint32 (they wrap modulo 2^32) and are read back as int32.
+__device__ __forceinline__ int32_t requant_nearest_even(int32_t v, int shift, int32_t lo, int32_t hi) {
+    const int64_t x = v;
+    int64_t q = x >> shift;                              // floor(x / 2^shift)
+    if (shift > 0) {
+        const int64_t r = x - (q << shift), half = int64_t(1) << (shift - 1);
+        if (r > half || (r == half && (q & 1))) ++q;
+    }
+    return int32_t(q < lo ? lo : (q > hi ? hi : q));
+}
+
+__device__ __forceinline__ uint16_t bf16_nearest_even(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return uint16_t((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+template <int DT, typename V>
+__device__ __forceinline__ void write_c(const KernelArgs &a, int64_t idx, V v) {
+    if constexpr (DT == DT_I8) {
+        const int32_t x = int32_t(v);
+        if (a.epilogue == EPI_I8)
+            static_cast<int8_t *>(a.C)[idx] = int8_t(requant_nearest_even(x, a.shift, -128, 127));
+        else if (a.epilogue == EPI_I16)
+            static_cast<int16_t *>(a.C)[idx] = int16_t(requant_nearest_even(x, a.shift, -32768, 32767));
+        else
+            static_cast<int32_t *>(a.C)[idx] = x;
+    } else {
+        const float x = float(v);
+        if (a.epilogue == EPI_BF16) static_cast<uint16_t *>(a.C)[idx] = bf16_nearest_even(x);
+        else static_cast<float *>(a.C)[idx] = x;
+    }
+}
+
 template <int DT, int BM, int BN, int TM, int TN>
 __device__ __forceinline__ void store_tile(const KernelArgs &args,
                                            const typename Types<DT>::acc_vec (&acc)[TM][TN],
@@ -143,11 +178,8 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
     const int frag_row = lane & 31, frag_half = lane >> 5;
     const int64_t M = args.M, N = args.N;
     const int64_t plane = M * N;
-    if (args.split_k == 1 || !args.reduce_in_kernel) {
-        // C itself, or this slice's partial plane for the separate reduction.
-        out_t *out = args.split_k > 1 ? static_cast<out_t *>(args.workspace) + int64_t(slice) * plane
-                                      : static_cast<out_t *>(args.C);
-        const int64_t ldo = args.split_k > 1 ? N : args.ldc;
+    if (args.split_k == 1) {
+        // C itself, through the call's output conversion.
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -156,7 +188,23 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                    if (row < M && col < N) out[row * ldo + col] = acc[i][j][r];
+                    if (row < M && col < N) write_c<DT>(args, row * args.ldc + col, acc[i][j][r]);
+                }
+            }
+        return;
+    }
+    if (!args.reduce_in_kernel) {
+        // This slice's partial plane for the separate reduction.
+        out_t *out = static_cast<out_t *>(args.workspace) + int64_t(slice) * plane;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                    if (row < M && col < N) out[row * N + col] = acc[i][j][r];
                 }
             }
         return;
@@ -191,7 +239,6 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
 
     // Last slice of this tile: C = ((ws[0] + ws[1]) + ws[2]) + ... over the valid part of the
     // tile, by all threads, consecutive columns per thread, with up to sixteen slices in flight.
-    out_t *C = static_cast<out_t *>(args.C);
     const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
     const int rows = int(M - m0 < BM ? M - m0 : BM);
     const int cols = int(N - n0 < BN ? N - n0 : BN);
@@ -218,10 +265,10 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
                     for (int e = 0; e < V; ++e) s[e] = (p0 + u == 0) ? v[u][e] : s[e] + v[u][e];
                 }
         }
-        out_t *dst = C + (m0 + rr) * args.ldc + n0 + cv;
+        const int64_t dst = (m0 + rr) * args.ldc + n0 + cv;
 #pragma unroll
         for (int e = 0; e < V; ++e)
-            if (e < nv) dst[e] = out_t(s[e]);
+            if (e < nv) write_c<DT>(args, dst + e, s[e]);
     }
     if (threadIdx.x == 0)
         __hip_atomic_store(&args.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1817,15 +1864,13 @@ using gemv_sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type
 template <int DT, int COLS>
 __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_acc_t<DT> *v, int64_t n0,
                                            int tile, int slice) {
-    using out_t = typename Types<DT>::out_t;
     using sum_t = gemv_sum_t<DT>;
     const int64_t N = args.N;
-    out_t *C = static_cast<out_t *>(args.C);
     sum_t *ws = static_cast<sum_t *>(args.workspace);
     const int t = int(threadIdx.x);
     if (args.split_k == 1) {
         for (int c = t; c < COLS; c += 256)
-            if (n0 + c < N) C[n0 + c] = out_t(v[c]);
+            if (n0 + c < N) write_c<DT>(args, n0 + c, v[c]);
         return;
     }
     if (!args.reduce_in_kernel) {
@@ -1859,7 +1904,7 @@ __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_ac
             for (int u = 0; u < 16; ++u)
                 if (p0 + u < args.split_k) s = (p0 + u == 0) ? v16[u] : s + v16[u];
         }
-        C[n0 + c] = out_t(s);
+        write_c<DT>(args, n0 + c, s);
     }
     if (t == 0) __hip_atomic_store(&args.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -2042,17 +2087,17 @@ __global__ __launch_bounds__(256) void gemv_bt_kernel(KernelArgs args) {
 
 // Sums split-K partials [split][M][N] into C in slice order 0, 1, ... (the
 // same fixed order as the in-kernel reduction).
-template <typename T>
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(const T *__restrict__ ws, int32_t split,
-                                                            int64_t M, int64_t N,
-                                                            T *__restrict__ C, int64_t ldc) {
-    const int64_t total = M * N;
+template <int DT>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(KernelArgs a) {
+    using sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;   // int32 wraps mod 2^32
+    const sum_t *__restrict__ ws = static_cast<const sum_t *>(a.workspace);
+    const int64_t total = a.M * a.N;
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
     for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total; idx += stride) {
-        T s = ws[idx];
-        for (int32_t p = 1; p < split; ++p) s += ws[int64_t(p) * total + idx];
-        const int64_t row = idx / N, col = idx % N;
-        C[row * ldc + col] = s;
+        sum_t s = ws[idx];
+        for (int32_t p = 1; p < a.split_k; ++p) s += ws[int64_t(p) * total + idx];
+        const int64_t row = idx / a.N, col = idx % a.N;
+        write_c<DT>(a, row * a.ldc + col, s);
     }
 }
 
@@ -2274,13 +2319,9 @@ int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr
         int64_t blocks = (total + 255) / 256;
         if (blocks > 8192) blocks = 8192;
         if (args.dtype == DT_I8)   // unsigned adds: int32 partials wrap modulo 2^32, defined
-            hipLaunchKernelGGL(splitk_reduce_kernel<uint32_t>, dim3(unsigned(blocks)), dim3(256), 0, stream,
-                               static_cast<const uint32_t *>(args.workspace), args.split_k, args.M, args.N,
-                               static_cast<uint32_t *>(args.C), args.ldc);
+            hipLaunchKernelGGL(splitk_reduce_kernel<DT_I8>, dim3(unsigned(blocks)), dim3(256), 0, stream, args);
         else
-            hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(unsigned(blocks)), dim3(256), 0, stream,
-                               static_cast<const float *>(args.workspace), args.split_k, args.M, args.N,
-                               static_cast<float *>(args.C), args.ldc);
+            hipLaunchKernelGGL(splitk_reduce_kernel<DT_BF16>, dim3(unsigned(blocks)), dim3(256), 0, stream, args);
         e = hipGetLastError();
     }
     return e == hipSuccess ? LAUNCH_OK : LAUNCH_HIP_ERROR;

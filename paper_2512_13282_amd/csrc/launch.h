@@ -21,7 +21,15 @@ struct KernelArgs {
     int32_t group_m;               // tile-rows per group in the launch order
     int32_t reduce_in_kernel;      // split-K: 1 = last slice of each tile sums it, 0 = separate kernel
     int32_t b_trans;               // 1: B is stored column-major (N x K, row stride ldb >= K)
+    int32_t epilogue;              // output conversion, EPI_* below
+    int32_t shift;                 // EPI_I8 / EPI_I16: results are divided by 2^shift
 };
+
+// Output conversions.  EPI_NONE writes the accumulator type (int32 / fp32).
+// EPI_I8 / EPI_I16: int32 result / 2^shift rounded to the nearest integer, ties
+// to even, saturated to the int8 / int16 range.  EPI_BF16: fp32 result rounded
+// to the nearest bf16, ties to even.
+enum { EPI_NONE = 0, EPI_I8 = 1, EPI_I16 = 2, EPI_BF16 = 3 };
 
 enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2 };
 

@@ -116,3 +116,21 @@ def test_bt_strides_follow_the_n_by_k_layout():
     with pytest.raises(b.GemmError):
         b.gemm_plan(I8, 64, 512, 128, 128, 128, 512, FAKE_A, FAKE_B, FAKE_C)
     assert b.gemm_i8_i32_bt(0, 5, 7, 0, 7, FAKE_B, 7, 0, 5, 0) == b.GEMM_OK
+
+
+@pytest.mark.parametrize("fn", [b.gemm_i8_i8, b.gemm_i8_i16, b.gemm_i8_i8_bt, b.gemm_i8_i16_bt])
+def test_requant_shift_range(fn):
+    for shift in (-1, 32, 1000):
+        assert fn(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4, shift, 0) == b.GEMM_ERR_INVALID_VALUE
+    assert fn(0, 4, 4, 0, 4, FAKE_B, 4, 0, 4, 31, 0) == b.GEMM_OK          # empty: no-op
+
+
+def test_reduced_output_alignment_and_overlap():
+    # int16 / bf16 outputs need 2-byte alignment, int8 outputs none
+    assert b.gemm_i8_i16(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C + 1, 4, 0, 0) == b.GEMM_ERR_INVALID_VALUE
+    assert b.gemm_bf16_bf16(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C + 1, 4, 0) == b.GEMM_ERR_INVALID_VALUE
+    # a 4 x 4 int8 C starting inside A overlaps it
+    assert b.gemm_i8_i8(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_A + 15, 4, 0, 0) == b.GEMM_ERR_INVALID_VALUE
+    assert b.gemm_i8_i16(4, 4, 4, FAKE_A + 8, 4, FAKE_B, 4, FAKE_A, 4, 0, 0) == b.GEMM_ERR_INVALID_VALUE
+    assert b.gemm_i8_i8(4, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 3, 0, 0) == b.GEMM_ERR_INVALID_VALUE  # ldc < N
+    assert b.gemm_bf16_bf16_bt(4, 8, 16, FAKE_A, 16, FAKE_B, 15, FAKE_C, 8, 0) == b.GEMM_ERR_INVALID_VALUE
