@@ -10,6 +10,10 @@ the CPU oracle timed on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--size S] [--sweep]
 
+`--paper-sweep` times the GEMM over every (M, K, N) in multiples of the 256 tile
+up to 8192 (512 points per dtype and B layout).  The default run also times the
+8192^3 GEMMs with narrowed outputs (int8 -> int8, bf16 -> bf16).
+
 `--sweep` also times every workload of the sweep (one JSON row each, on
 stderr and in gpurun_out/sweep.jsonl); memory-bound shapes there rotate
 through enough copies of B to defeat the 256 MB last-level cache.  The same
@@ -35,6 +39,7 @@ HBM_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2512_13282_amd", "csrc", "gemm_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 COPY_PROBE_BYTES = 512 * 1024 * 1024
+REQUANT_SHIFT = 14          # int8 -> int8 output: results / 2^14 (|C| <= 2^21 at K = 8192 for uniform int8)
 
 
 def parse():
@@ -54,6 +59,12 @@ def parse():
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
                     help="write profiles/traffic.json from two rocprofv3 --pmc counter CSVs "
                          "(FETCH_SIZE, WRITE_SIZE) of a `bench.py --copy-probe` run, then exit")
+    ap.add_argument("--no-reduced", action="store_true",
+                    help="skip the reduced-precision-output measurements (int8 -> int8, bf16 -> bf16)")
+    ap.add_argument("--paper-sweep", action="store_true",
+                    help="also time the GEMM over M, K, N in multiples of the 256 tile up to 8192, both "
+                         "dtypes and B layouts (the paper's > 400-size sweep); details in "
+                         "gpurun_out/paper_sweep.jsonl, summary in the JSON line")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 512 MiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -80,10 +91,11 @@ class Workload:
     """One GEMM with its operands resident on the GPU.  bt=True stores B column-major
     (as Bt, N x K) and calls the *_bt entry points."""
 
-    def __init__(self, dtype, M, N, K, copies=1, seed=0, bt=False):
+    def __init__(self, dtype, M, N, K, copies=1, seed=0, bt=False, out="native"):
         import torch
         from paper_2512_13282_amd import binding, inputs
         self.dtype, self.M, self.N, self.K, self.bt = dtype, M, N, K, bt
+        self.out = out      # "native" (int32 / fp32 C), "i8" (int8 -> int8, shift) or "bf16" (bf16 -> bf16)
         self.b = binding
         A, B = inputs.make_inputs(dtype, M, N, K, seed=seed)
         self.A_host, self.B_host = A, B
@@ -94,11 +106,19 @@ class Workload:
         Bdev = to(np.ascontiguousarray(B.T)) if bt else to(B)
         self.dBs = [Bdev] + [Bdev.clone() for _ in range(copies - 1)]
         self.ldb = K if bt else N
-        self.dC = torch.empty((M, N), dtype=torch.int32 if dtype == "int8" else torch.float32, device=dev)
-        if bt:
-            self.fn = binding.gemm_i8_i32_bt if dtype == "int8" else binding.gemm_bf16_f32_bt
+        c_dtype = {"native": torch.int32 if dtype == "int8" else torch.float32, "i8": torch.int8,
+                   "bf16": torch.int16}[out]
+        self.dC = torch.empty((M, N), dtype=c_dtype, device=dev)
+        sfx = "_bt" if bt else ""
+        if out == "native":
+            self.fn = getattr(binding, ("gemm_i8_i32" if dtype == "int8" else "gemm_bf16_f32") + sfx)
+        elif out == "i8":
+            assert dtype == "int8"
+            f = getattr(binding, "gemm_i8_i8" + sfx)
+            self.fn = lambda *a: f(*a[:-1], REQUANT_SHIFT, a[-1])
         else:
-            self.fn = binding.gemm_i8_i32 if dtype == "int8" else binding.gemm_bf16_f32
+            assert dtype == "bf16"
+            self.fn = getattr(binding, "gemm_bf16_bf16" + sfx)
         self.stream = torch.cuda.current_stream(dev)
         self.i = 0
 
@@ -137,7 +157,8 @@ def time_workload(w: Workload, steps: int, warmup: int):
 def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
     ops = 2.0 * w.M * w.N * w.K
     e = 1 if w.dtype == "int8" else 2
-    comp_bytes = w.M * w.K * e + w.K * w.N * e + w.M * w.N * 4
+    c_bytes = {"native": 4, "i8": 1, "bf16": 2}[getattr(w, "out", "native")]
+    comp_bytes = w.M * w.K * e + w.K * w.N * e + w.M * w.N * c_bytes
     plan = w.plan()
     value = ops / (ms_step * 1e-3) / 1e12
     achieved = ops / (k_avg * 1e-3) / 1e12
@@ -168,7 +189,16 @@ def parity_sample(w: Workload, rows):
     Ar = np.ascontiguousarray(w.A_host[rows])
     if w.dtype == "int8":
         ref, ovf = o.gemm_i8_i32(Ar, w.B_host)
+        if w.out == "i8":
+            ref = o.requant_i32(ref, REQUANT_SHIFT, 8)
         return bool(ovf == 0 and np.array_equal(C, ref))
+    if w.out == "bf16":
+        # within one bf16 step of the correctly rounded exact result
+        from paper_2512_13282_amd import inputs
+        ref = inputs.f32_from_bf16_bits(o.round_bf16(o.gemm_bf16_f64(Ar, w.B_host))).astype(np.float64)
+        got = inputs.f32_from_bf16_bits(C.view(np.uint16)).astype(np.float64)
+        step = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -126))) - 7)
+        return bool(np.all(np.abs(got - ref) <= step))
     from paper_2512_13282_amd import inputs
     ref = o.gemm_bf16_f64(Ar, w.B_host)
     err = oracle.normalized_error(C, ref, w.K, float(np.abs(inputs.f32_from_bf16_bits(w.A_host)).max()),
@@ -302,6 +332,72 @@ def write_traffic(fetch_csv: str, write_csv: str) -> None:
     print(json.dumps(out, indent=2))
 
 
+PAPER_SWEEP_SIZES = (256, 512, 1024, 2048, 3072, 4096, 6144, 8192)
+
+
+def paper_sweep_run(iters: int = 5) -> dict:
+    """GEMM TOPS over every (M, K, N) in PAPER_SWEEP_SIZES^3 (multiples of the 256 tile up to
+    8192), both dtypes and both B layouts, with the selector's plans.  Operands are drawn on the
+    device (torch, seed 0) in the sweep's distributions and reused as views; each point is the
+    median of `iters` HIP-event-timed launches after two warm-ups.  Returns a summary; every
+    point goes to gpurun_out/paper_sweep.jsonl."""
+    import torch
+    from paper_2512_13282_amd import binding
+    dev = torch.device("cuda:0")
+    torch.manual_seed(0)
+    S = max(PAPER_SWEEP_SIZES)
+    st = torch.cuda.current_stream(dev)
+    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+    summary = {"sizes": list(PAPER_SWEEP_SIZES), "points_per_series": len(PAPER_SWEEP_SIZES) ** 3}
+    with open(os.path.join(ROOT, "gpurun_out", "paper_sweep.jsonl"), "w") as f:
+        for dtype in ("int8", "bf16"):
+            if dtype == "int8":
+                A = torch.randint(-128, 128, (S * S,), dtype=torch.int8, device=dev)
+                B = torch.randint(-128, 128, (S * S,), dtype=torch.int8, device=dev)
+                C = torch.empty(S * S, dtype=torch.int32, device=dev)
+            else:
+                A = torch.randn(S * S, device=dev).to(torch.bfloat16)
+                B = torch.randn(S * S, device=dev).to(torch.bfloat16)
+                C = torch.empty(S * S, dtype=torch.float32, device=dev)
+            for bt in (False, True):
+                fn = getattr(binding, ("gemm_i8_i32" if dtype == "int8" else "gemm_bf16_f32") + ("_bt" if bt else ""))
+                tops = []
+                for M in PAPER_SWEEP_SIZES:
+                    for K in PAPER_SWEEP_SIZES:
+                        for N in PAPER_SWEEP_SIZES:
+                            ldb = K if bt else N
+                            call = lambda: fn(M, N, K, A.data_ptr(), K, B.data_ptr(), ldb, C.data_ptr(), N,
+                                              st.cuda_stream)
+                            for _ in range(2):
+                                if call() != 0:
+                                    raise RuntimeError(f"GEMM failed at {(dtype, M, K, N, bt)}")
+                            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                                  for _ in range(iters)]
+                            for a, b in ev:
+                                a.record(st)
+                                call()
+                                b.record(st)
+                            torch.cuda.synchronize()
+                            ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+                            t = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+                            tops.append((t, M, K, N))
+                            f.write(json.dumps({"dtype": dtype, "b_layout": "col" if bt else "row", "M": M,
+                                                "K": K, "N": N, "kernel_ms": round(ms, 5),
+                                                "tops": round(t, 2)}) + "\n")
+                vals = np.array([x[0] for x in tops])
+                best = max(tops)
+                key = f"{dtype}_{'col' if bt else 'row'}_major_b"
+                summary[key] = {"max": round(best[0], 1), "max_at_MKN": list(best[1:]),
+                                "median": round(float(np.median(vals)), 1),
+                                "points_at_or_above_40pct_peak": int(np.sum(vals >= 0.4 * PEAK[dtype])),
+                                "unit": "TOPS" if dtype == "int8" else "TFLOP/s"}
+                print(f"[paper-sweep] {key}: max {best[0]:.1f} at M,K,N={best[1:]}, median "
+                      f"{np.median(vals):.1f}", file=sys.stderr, flush=True)
+            del A, B, C
+            torch.cuda.empty_cache()
+    return summary
+
+
 def main():
     args = parse()
     if args.traffic_from:
@@ -347,6 +443,24 @@ def main():
             print(f"[bench] {dtype} {S}^3 column-major B: {r['value']} {r['unit']} ({r['pct_dense_peak']}% of "
                   f"dense peak), kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
             del w
+
+    reduced = {}
+    if not args.no_reduced:
+        for dtype, out in (("int8", "i8"), ("bf16", "bf16")):
+            if args.only is not None and args.only != dtype:
+                continue
+            w = Workload(dtype, S, S, S, out=out)
+            ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+            r = summarize(w, ms, kavg, kmin)
+            r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
+            key = "int8_to_int8" if dtype == "int8" else "bf16_to_bf16"
+            reduced[key] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg", "pct_dense_peak",
+                                              "plan", "split_k", "parity_sample_ok", "roofline")}
+            print(f"[bench] {key} {S}^3: {r['value']} {r['unit']} ({r['pct_dense_peak']}% of dense peak), "
+                  f"kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
+            del w
+
+    paper_sweep = paper_sweep_run() if args.paper_sweep else None
 
     if args.copy_probe:
         # Elementwise copy of 512 MiB: reads 512 MiB, writes 512 MiB.  Profiled beside the
@@ -419,6 +533,12 @@ def main():
     if bt_results:
         line["column_major_b"] = {"workload": f"the same GEMMs with B stored column-major (N x K), "
                                               f"gemm_*_bt entry points", **bt_results}
+    if reduced:
+        line["reduced_outputs"] = {"workload": f"the same {S}^3 GEMMs with narrowed outputs: int8 -> int8 "
+                                               f"(results / 2^{REQUANT_SHIFT}, nearest-even, saturated) and "
+                                               f"bf16 -> bf16 (nearest-even)", **reduced}
+    if paper_sweep is not None:
+        line["paper_sweep"] = paper_sweep
     print(json.dumps(line), flush=True)
 
 
