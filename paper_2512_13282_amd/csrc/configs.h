@@ -83,6 +83,9 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,      64, 256, 1, 4, 1, 6, 0.22, 0.26, 1, "ring_64x256_w4"},
     {FAM_GEMV,       1, 1024, 1, 4, 4, 1, 0.03, 0.06, 0, "gemv_1024"},
     {FAM_GEMV,       1,  16, 1, 4, 4, 1, 0.03, 0.06, 1, "gemv_bt_16"},
+    {FAM_RING,      32, 256, 1, 4, 2, 4, 0.15, 0.18, 1, "ring_32x256_w4_r4"},
+    {FAM_RING,      32, 128, 1, 4, 2, 6, 0.12, 0.14, 1, "ring_32x128_w4_r6"},
+    {FAM_RING,      64, 128, 1, 4, 2, 5, 0.18, 0.20, 1, "ring_64x128_w4_r5"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

@@ -2165,6 +2165,9 @@ static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t gri
         case 23: return launch_ring<DT, 64, 128, 1, 4, 2, 8>(a, grid, s);
         case 24: return launch_ring<DT, 32, 256, 1, 4, 1, 6>(a, grid, s);
         case 25: return launch_ring<DT, 64, 256, 1, 4, 1, 6>(a, grid, s);
+        case 28: return launch_ring<DT, 32, 256, 1, 4, 2, 4>(a, grid, s);
+        case 29: return launch_ring<DT, 32, 128, 1, 4, 2, 6>(a, grid, s);
+        case 30: return launch_ring<DT, 64, 128, 1, 4, 2, 5>(a, grid, s);
         case 27:
             hipLaunchKernelGGL((gemv_bt_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
@@ -2199,6 +2202,7 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
             hipLaunchKernelGGL((gemm_stream_kernel<DT, 64, 3>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
         case 16: case 17: case 18: case 19: case 20: case 21: case 22: case 23: case 24: case 25:
+        case 28: case 29: case 30:
             return launch_config_bt<DT>(cfg, a, grid, s);   // the ring kernels take either B layout
         case 26:
             hipLaunchKernelGGL((gemv_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
