@@ -86,6 +86,9 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,      32, 256, 1, 4, 2, 4, 0.15, 0.18, 1, "ring_32x256_w4_r4"},
     {FAM_RING,      32, 128, 1, 4, 2, 6, 0.12, 0.14, 1, "ring_32x128_w4_r6"},
     {FAM_RING,      64, 128, 1, 4, 2, 5, 0.18, 0.20, 1, "ring_64x128_w4_r5"},
+    {FAM_RING,     128, 128, 2, 2, 2, 4, 0.30, 0.34, 1, "ring_128x128_w4"},
+    {FAM_RING,     128, 128, 2, 2, 1, 8, 0.30, 0.34, 1, "ring_128x128_w4_r8"},
+    {FAM_RING,     128, 128, 2, 4, 1, 8, 0.30, 0.34, 1, "ring_128x128_w8"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

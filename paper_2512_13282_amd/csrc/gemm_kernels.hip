@@ -1166,15 +1166,14 @@ __device__ __forceinline__ i32x4_t ring_rsrc(const uint8_t *base, uint32_t bytes
 // tell the ring buffers apart and would wait for every load in flight before each
 // read); completion is tracked by the explicit vmcnt waits of the ring instead,
 // and nothing else in the kernel accesses the ring.
+// The LDS address goes in M0, which the "{m0}" operand has the compiler load.
 __device__ __forceinline__ void ring_load16(i32x4_t rsrc, uint32_t lds, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :: "v"(voff), "s"(rsrc), "s"(lds) : "memory", "m0");
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" :: "v"(voff), "s"(rsrc), "{m0}"(lds) : "memory");
 }
 
 // The same with 4 bytes per lane: lane l's dword lands at LDS byte lds + 4 l.
 __device__ __forceinline__ void ring_load4(i32x4_t rsrc, uint32_t lds, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
-                 :: "v"(voff), "s"(rsrc), "s"(lds) : "memory", "m0");
+    asm volatile("buffer_load_dword %0, %1, 0 offen lds" :: "v"(voff), "s"(rsrc), "{m0}"(lds) : "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
@@ -2168,6 +2167,9 @@ static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t gri
         case 28: return launch_ring<DT, 32, 256, 1, 4, 2, 4>(a, grid, s);
         case 29: return launch_ring<DT, 32, 128, 1, 4, 2, 6>(a, grid, s);
         case 30: return launch_ring<DT, 64, 128, 1, 4, 2, 5>(a, grid, s);
+        case 31: return launch_ring<DT, 128, 128, 2, 2, 2, 4>(a, grid, s);
+        case 32: return launch_ring<DT, 128, 128, 2, 2, 2, 8>(a, grid, s);
+        case 33: return launch_ring<DT, 128, 128, 2, 4, 2, 8>(a, grid, s);
         case 27:
             hipLaunchKernelGGL((gemv_bt_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
@@ -2202,7 +2204,7 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
             hipLaunchKernelGGL((gemm_stream_kernel<DT, 64, 3>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
         case 16: case 17: case 18: case 19: case 20: case 21: case 22: case 23: case 24: case 25:
-        case 28: case 29: case 30:
+        case 28: case 29: case 30: case 31: case 32: case 33:
             return launch_config_bt<DT>(cfg, a, grid, s);   // the ring kernels take either B layout
         case 26:
             hipLaunchKernelGGL((gemv_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
