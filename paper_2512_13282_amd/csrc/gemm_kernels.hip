@@ -1675,12 +1675,6 @@ void gemm_pingpong_kernel(KernelArgs args) {
 // of the slice are still issued (zero-size resource: they return zero without
 // touching memory) so that every iteration counts the same loads.
 // ---------------------------------------------------------------------------
-template <int VMCNT>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(VMCNT >= 0 && VMCNT < 64, "vmcnt range");
-    // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
-    __builtin_amdgcn_s_waitcnt((VMCNT & 15) | (7 << 4) | (15 << 8) | ((VMCNT >> 4) << 14));
-}
 
 template <int DT, int BM, int NS>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
@@ -1742,19 +1736,25 @@ void gemm_stream_kernel(KernelArgs args) {
     const uint8_t *const b_base = static_cast<const uint8_t *>(args.B) + (k_begin * args.ldb + n0) * E;
     const int64_t k_len = k_end - k_begin;
 
+    // The loads are the ring kernel's inline-assembly form, invisible to the compiler's
+    // wait-count tracking (which cannot tell the stage buffers apart and would make every
+    // fragment read wait for all loads in flight); the explicit vmcnt wait before each
+    // barrier accounts for them.
+    const uint32_t wave_u = uint32_t(__builtin_amdgcn_readfirstlane(wave));
     auto load_stage = [&](int kt, auto buf_c) {
         constexpr int BUF = decltype(buf_c)::value;
         const int64_t rem = k_len - int64_t(kt) * BK;
-        const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_base + int64_t(kt) * kStageKBytes, rem > 0 ? a_bytes : 0u);
+        const i32x4_t ra = ring_rsrc(a_base + int64_t(kt) * kStageKBytes, rem > 0 ? a_bytes : 0u);
         const int64_t rows = rem <= 0 ? 0 : (rem < BK ? rem : BK);
-        const __amdgpu_buffer_rsrc_t rb = make_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
+        const i32x4_t rb = ring_rsrc(b_base + int64_t(kt) * BK * ldb_b, uint32_t(rows * ldb_b));
 #pragma unroll
         for (int i = 0; i < A_INSTR; ++i) {
             const uint32_t off = int64_t(a_chunk[i]) * VECE < rem ? a_voff[i] : kOOB;
-            load_lds16(ra, &a_lds[BUF][(i * WAVES + wave) * 1024], off);
+            ring_load16(ra, lds_addr(&a_lds[BUF][0]) + (i * WAVES + wave_u) * 1024, off);
         }
 #pragma unroll
-        for (int i = 0; i < B_INSTR; ++i) load_lds16(rb, &b_lds[BUF][(i * WAVES + wave) * 1024], b_voff[i]);
+        for (int i = 0; i < B_INSTR; ++i)
+            ring_load16(rb, lds_addr(&b_lds[BUF][0]) + (i * WAVES + wave_u) * 1024, b_voff[i]);
     };
 
     const int frag_row = lane & 31;
@@ -1811,8 +1811,8 @@ void gemm_stream_kernel(KernelArgs args) {
     // One iteration: stage kt is in buffer BUF; buffer (BUF + NS - 1) % NS receives stage kt + NS - 1.
     auto iteration = [&](int kt, auto buf_c) {
         constexpr int BUF = decltype(buf_c)::value;
-        wait_vmcnt<(NS - 2) * LPS>();                      // own loads of stage kt have landed
-        __syncthreads();                                   // everyone's; buffer BUF-1 retired
+        ring_barrier<(NS - 2) * LPS>();                    // own loads of stage kt have landed, then
+                                                           // everyone's; buffer BUF-1 retired
         load_stage(kt + NS - 1, std::integral_constant<int, (BUF + NS - 1) % NS>{});
         compute(buf_c);
     };
