@@ -89,6 +89,9 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,     128, 128, 2, 2, 2, 4, 0.30, 0.34, 1, "ring_128x128_w4"},
     {FAM_RING,     128, 128, 2, 2, 1, 8, 0.30, 0.34, 1, "ring_128x128_w4_r8"},
     {FAM_RING,     128, 128, 2, 4, 1, 8, 0.30, 0.34, 1, "ring_128x128_w8"},
+    {FAM_RING,     256, 256, 4, 2, 1, 5, 0.40, 0.45, 1, "ring_256x256_w8t_r5"},
+    {FAM_RING,     256, 256, 2, 4, 1, 5, 0.40, 0.45, 1, "ring_256x256_w8_r5"},
+    {FAM_RING,     256, 256, 2, 2, 1, 5, 0.38, 0.42, 1, "ring_256x256_w4_r5"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

@@ -152,27 +152,67 @@ __device__ __forceinline__ uint16_t bf16_nearest_even(float f) {
     return uint16_t((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
-template <int DT, typename V>
-__device__ __forceinline__ void write_c(const KernelArgs &a, int64_t idx, V v) {
+template <int DT, int EPI, typename V>
+__device__ __forceinline__ void write_c_as(const KernelArgs &a, int64_t idx, V v) {
     if constexpr (DT == DT_I8) {
         const int32_t x = int32_t(v);
-        if (a.epilogue == EPI_I8)
+        if constexpr (EPI == EPI_I8)
             static_cast<int8_t *>(a.C)[idx] = int8_t(requant_nearest_even(x, a.shift, -128, 127));
-        else if (a.epilogue == EPI_I16)
+        else if constexpr (EPI == EPI_I16)
             static_cast<int16_t *>(a.C)[idx] = int16_t(requant_nearest_even(x, a.shift, -32768, 32767));
         else
             static_cast<int32_t *>(a.C)[idx] = x;
     } else {
         const float x = float(v);
-        if (a.epilogue == EPI_BF16) static_cast<uint16_t *>(a.C)[idx] = bf16_nearest_even(x);
+        if constexpr (EPI == EPI_BF16) static_cast<uint16_t *>(a.C)[idx] = bf16_nearest_even(x);
         else static_cast<float *>(a.C)[idx] = x;
     }
 }
 
+template <int DT, typename V>
+__device__ __forceinline__ void write_c(const KernelArgs &a, int64_t idx, V v) {
+    if constexpr (DT == DT_I8) {
+        if (a.epilogue == EPI_I8) write_c_as<DT, EPI_I8>(a, idx, v);
+        else if (a.epilogue == EPI_I16) write_c_as<DT, EPI_I16>(a, idx, v);
+        else write_c_as<DT, EPI_NONE>(a, idx, v);
+    } else {
+        if (a.epilogue == EPI_BF16) write_c_as<DT, EPI_BF16>(a, idx, v);
+        else write_c_as<DT, EPI_NONE>(a, idx, v);
+    }
+}
+
+// A wave's output fragments straight into C with the epilogue EPI.  The epilogue
+// is a template argument so that the fully unrolled loops stay small enough to
+// unroll: the accumulators are then only ever indexed by constants and stay in
+// registers (a 256-register accumulator tile would otherwise go to scratch).
+template <int DT, int EPI, int TM, int TN>
+__device__ __forceinline__ void store_c_direct(const KernelArgs &args,
+                                               const typename Types<DT>::acc_vec (&acc)[TM][TN],
+                                               int64_t r0, int64_t c0, int lane) {
+    const int frag_row = lane & 31, frag_half = lane >> 5;
+    const int64_t M = args.M, N = args.N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                if (row < M && col < N) write_c_as<DT, EPI>(args, row * args.ldc + col, acc[i][j][r]);
+            }
+        }
+}
+
+// s_last: one int of LDS for the in-kernel split-K reduction's "last slice"
+// broadcast; a kernel whose LDS is otherwise free at this point may lend it a word
+// of its operand buffers (all of its global -> LDS loads complete, all of its
+// fragment reads done).
 template <int DT, int BM, int BN, int TM, int TN>
 __device__ __forceinline__ void store_tile(const KernelArgs &args,
                                            const typename Types<DT>::acc_vec (&acc)[TM][TN],
-                                           int tm, int tn, int slice, int64_t r0, int64_t c0, int lane) {
+                                           int tm, int tn, int slice, int64_t r0, int64_t c0, int lane,
+                                           int &s_last) {
     using out_t = typename Types<DT>::out_t;
     using sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;  // int32 wraps mod 2^32
     const int frag_row = lane & 31, frag_half = lane >> 5;
@@ -180,17 +220,14 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
     const int64_t plane = M * N;
     if (args.split_k == 1) {
         // C itself, through the call's output conversion.
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int64_t col = c0 + j * 32 + frag_row;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                    if (row < M && col < N) write_c<DT>(args, row * args.ldc + col, acc[i][j][r]);
-                }
-            }
+        if constexpr (DT == DT_I8) {
+            if (args.epilogue == EPI_I8) store_c_direct<DT, EPI_I8>(args, acc, r0, c0, lane);
+            else if (args.epilogue == EPI_I16) store_c_direct<DT, EPI_I16>(args, acc, r0, c0, lane);
+            else store_c_direct<DT, EPI_NONE>(args, acc, r0, c0, lane);
+        } else {
+            if (args.epilogue == EPI_BF16) store_c_direct<DT, EPI_BF16>(args, acc, r0, c0, lane);
+            else store_c_direct<DT, EPI_NONE>(args, acc, r0, c0, lane);
+        }
         return;
     }
     if (!args.reduce_in_kernel) {
@@ -225,7 +262,6 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
                 }
             }
     }
-    __shared__ int s_last;
     const int tile = tm * args.tiles_n + tn;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's partial stores are complete
     __syncthreads();                                   // ... and every thread's
@@ -571,7 +607,8 @@ void gemm_tile_kernel(KernelArgs args) {
     }
 
     // ---------------- epilogue ----------------
-    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
+    __shared__ int s_last;
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane, s_last);
 }
 
 // ---------------------------------------------------------------------------
@@ -785,7 +822,8 @@ void gemm_vec_kernel(KernelArgs args) {
     }
     if (kt < nk) compute(0);
 
-    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
+    __shared__ int s_last;
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane, s_last);
 }
 
 // ---------------------------------------------------------------------------
@@ -1116,7 +1154,8 @@ void gemm_lds_kernel(KernelArgs args) {
     if (kt < nk) stage(kt, I0{});
     mfma_slot(I1{});
 
-    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
+    __shared__ int s_last;
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane, s_last);
 }
 
 // ---------------------------------------------------------------------------
@@ -1441,7 +1480,10 @@ void gemm_ring_kernel(KernelArgs args) {
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // drain ring loads past the end before exit
 
-    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
+    // The ring is drained and every wave is past its last fragment read when
+    // store_tile first synchronises, so it lends the last-slice flag a word.
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane,
+                                   *reinterpret_cast<int *>(ring_lds[0]));
 }
 
 // ---------------------------------------------------------------------------
@@ -1661,7 +1703,8 @@ void gemm_pingpong_kernel(KernelArgs args) {
         if (grp == 1) compute_unit();                       // group 1's last unit
     }
 
-    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane);
+    __shared__ int s_last;
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane, s_last);
 }
 
 // ---------------------------------------------------------------------------
@@ -1827,7 +1870,8 @@ void gemm_stream_kernel(KernelArgs args) {
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // drain ring loads past the end before exit
 
-    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0, n0 + wcol0, lane);
+    __shared__ int s_last;
+    store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0, n0 + wcol0, lane, s_last);
 }
 
 // ---------------------------------------------------------------------------
@@ -2170,6 +2214,9 @@ static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t gri
         case 31: return launch_ring<DT, 128, 128, 2, 2, 2, 4>(a, grid, s);
         case 32: return launch_ring<DT, 128, 128, 2, 2, 2, 8>(a, grid, s);
         case 33: return launch_ring<DT, 128, 128, 2, 4, 2, 8>(a, grid, s);
+        case 34: return launch_ring<DT, 256, 256, 4, 2, 2, 5>(a, grid, s);
+        case 35: return launch_ring<DT, 256, 256, 2, 4, 2, 5>(a, grid, s);
+        case 36: return launch_ring<DT, 256, 256, 2, 2, 1, 5>(a, grid, s);
         case 27:
             hipLaunchKernelGGL((gemv_bt_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
@@ -2204,7 +2251,7 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
             hipLaunchKernelGGL((gemm_stream_kernel<DT, 64, 3>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
         case 16: case 17: case 18: case 19: case 20: case 21: case 22: case 23: case 24: case 25:
-        case 28: case 29: case 30: case 31: case 32: case 33:
+        case 28: case 29: case 30: case 31: case 32: case 33: case 34: case 35: case 36:
             return launch_config_bt<DT>(cfg, a, grid, s);   // the ring kernels take either B layout
         case 26:
             hipLaunchKernelGGL((gemv_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
