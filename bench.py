@@ -15,7 +15,7 @@ up to 8192 (512 points per dtype and B layout).  `--reduced` also times the 8192
 GEMMs with narrowed outputs (int8 -> int8, bf16 -> bf16).
 
 `--sweep` also times every workload of the sweep (one JSON row each, on
-stderr and in gpurun_out/sweep.jsonl); memory-bound shapes there rotate
+stderr and in OUT_DIR/sweep.jsonl); memory-bound shapes there rotate
 through enough copies of B to defeat the 256 MB last-level cache.  The same
 two 8192^3 GEMMs with B stored column-major (the *_bt entry points) are timed
 too and reported in the `column_major_b` object (`--no-bt` skips them).
@@ -68,7 +68,10 @@ def parse():
     ap.add_argument("--paper-sweep", action="store_true",
                     help="also time the GEMM over M, K, N in multiples of the 256 tile up to 8192, both "
                          "dtypes and B layouts (the paper's > 400-size sweep); details in "
-                         "gpurun_out/paper_sweep.jsonl, summary in the JSON line")
+                         "OUT_DIR/paper_sweep.jsonl, summary in the JSON line")
+    ap.add_argument("--out-dir", default="bench_out",
+                    help="directory (relative to the repository root unless absolute) for the "
+                         "per-point files of --sweep and --paper-sweep")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 512 MiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -344,21 +347,21 @@ def write_traffic(fetch_csv: str, write_csv: str) -> None:
 PAPER_SWEEP_SIZES = (256, 512, 1024, 2048, 3072, 4096, 6144, 8192)
 
 
-def paper_sweep_run(iters: int = 5) -> dict:
+def paper_sweep_run(out_dir: str, iters: int = 5) -> dict:
     """GEMM TOPS over every (M, K, N) in PAPER_SWEEP_SIZES^3 (multiples of the 256 tile up to
     8192), both dtypes and both B layouts, with the selector's plans.  Operands are drawn on the
     device (torch, seed 0) in the sweep's distributions and reused as views; each point is the
     median of `iters` HIP-event-timed launches after two warm-ups.  Returns a summary; every
-    point goes to gpurun_out/paper_sweep.jsonl."""
+    point goes to out_dir/paper_sweep.jsonl."""
     import torch
     from paper_2512_13282_amd import binding
     dev = torch.device("cuda:0")
     torch.manual_seed(0)
     S = max(PAPER_SWEEP_SIZES)
     st = torch.cuda.current_stream(dev)
-    os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+    os.makedirs(os.path.join(ROOT, out_dir), exist_ok=True)
     summary = {"sizes": list(PAPER_SWEEP_SIZES), "points_per_series": len(PAPER_SWEEP_SIZES) ** 3}
-    with open(os.path.join(ROOT, "gpurun_out", "paper_sweep.jsonl"), "w") as f:
+    with open(os.path.join(ROOT, out_dir, "paper_sweep.jsonl"), "w") as f:
         for dtype in ("int8", "bf16"):
             if dtype == "int8":
                 A = torch.randint(-128, 128, (S * S,), dtype=torch.int8, device=dev)
@@ -469,7 +472,7 @@ def main():
                   f"kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
             del w
 
-    paper_sweep = paper_sweep_run() if args.paper_sweep else None
+    paper_sweep = paper_sweep_run(args.out_dir) if args.paper_sweep else None
 
     if args.copy_probe:
         # Elementwise copy of 512 MiB: reads 512 MiB, writes 512 MiB.  Profiled beside the
@@ -483,8 +486,8 @@ def main():
 
     if args.sweep:
         from paper_2512_13282_amd import inputs
-        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
-        with open(os.path.join(ROOT, "gpurun_out", "sweep.jsonl"), "w") as f:
+        os.makedirs(os.path.join(ROOT, args.out_dir), exist_ok=True)
+        with open(os.path.join(ROOT, args.out_dir, "sweep.jsonl"), "w") as f:
             for (dtype, M, K, N) in inputs.ALL_CONFIGS:
                 e = 1 if dtype == "int8" else 2
                 bbytes = K * N * e
