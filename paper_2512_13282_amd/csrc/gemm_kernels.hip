@@ -152,21 +152,26 @@ __device__ __forceinline__ uint16_t bf16_nearest_even(float f) {
     return uint16_t((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Element type of C under epilogue EPI.
+template <int DT, int EPI> struct OutElem { using type = typename Types<DT>::out_t; };
+template <> struct OutElem<DT_I8, EPI_I8> { using type = int8_t; };
+template <> struct OutElem<DT_I8, EPI_I16> { using type = int16_t; };
+template <> struct OutElem<DT_BF16, EPI_BF16> { using type = uint16_t; };
+
+template <int DT, int EPI>
+__device__ __forceinline__ typename OutElem<DT, EPI>::type convert_out(const KernelArgs &a,
+                                                                         typename Types<DT>::out_t v) {
+    if constexpr (DT == DT_I8 && EPI == EPI_I8) return int8_t(requant_nearest_even(int32_t(v), a.shift, -128, 127));
+    else if constexpr (DT == DT_I8 && EPI == EPI_I16)
+        return int16_t(requant_nearest_even(int32_t(v), a.shift, -32768, 32767));
+    else if constexpr (DT == DT_BF16 && EPI == EPI_BF16) return bf16_nearest_even(float(v));
+    else return v;
+}
+
 template <int DT, int EPI, typename V>
 __device__ __forceinline__ void write_c_as(const KernelArgs &a, int64_t idx, V v) {
-    if constexpr (DT == DT_I8) {
-        const int32_t x = int32_t(v);
-        if constexpr (EPI == EPI_I8)
-            static_cast<int8_t *>(a.C)[idx] = int8_t(requant_nearest_even(x, a.shift, -128, 127));
-        else if constexpr (EPI == EPI_I16)
-            static_cast<int16_t *>(a.C)[idx] = int16_t(requant_nearest_even(x, a.shift, -32768, 32767));
-        else
-            static_cast<int32_t *>(a.C)[idx] = x;
-    } else {
-        const float x = float(v);
-        if constexpr (EPI == EPI_BF16) static_cast<uint16_t *>(a.C)[idx] = bf16_nearest_even(x);
-        else static_cast<float *>(a.C)[idx] = x;
-    }
+    static_cast<typename OutElem<DT, EPI>::type *>(a.C)[idx] =
+        convert_out<DT, EPI>(a, typename Types<DT>::out_t(v));
 }
 
 template <int DT, typename V>
@@ -181,27 +186,39 @@ __device__ __forceinline__ void write_c(const KernelArgs &a, int64_t idx, V v) {
     }
 }
 
-// A wave's output fragments straight into C with the epilogue EPI.  The epilogue
-// is a template argument so that the fully unrolled loops stay small enough to
-// unroll: the accumulators are then only ever indexed by constants and stay in
-// registers (a 256-register accumulator tile would otherwise go to scratch).
+// A wave's output fragments straight into C with the epilogue EPI.  Lane l holds,
+// for fragment (i, j) and register r, row r0 + 4 (l / 32) + 32 i + 8 (r / 4) + r % 4
+// and column c0 + l % 32 + 32 j: one base pointer per lane plus a row offset that
+// is a constant times ldc, which the scalar unit forms.  The epilogue is a template
+// argument so that the loop bodies stay small enough to unroll fully: the
+// accumulators are then only indexed by constants and stay in registers (with a
+// run-time choice per element, the 256-register tiles of the 4-wave 256 x 256
+// int8 kernels went to scratch).
 template <int DT, int EPI, int TM, int TN>
 __device__ __forceinline__ void store_c_direct(const KernelArgs &args,
                                                const typename Types<DT>::acc_vec (&acc)[TM][TN],
                                                int64_t r0, int64_t c0, int lane) {
-    const int frag_row = lane & 31, frag_half = lane >> 5;
-    const int64_t M = args.M, N = args.N;
+    using o_t = typename OutElem<DT, EPI>::type;
+    const int64_t row0 = r0 + 4 * (lane >> 5);
+    const int64_t col = c0 + (lane & 31);
+    const int64_t rows_left = args.M - row0;
+    const int64_t ldc = args.ldc;
+    o_t *const base = static_cast<o_t *>(args.C) + row0 * ldc + col;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int j = 0; j < TN; ++j) {
+        if (col + 32 * j >= args.N) continue;
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = c0 + j * 32 + frag_row;
+        for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
-                if (row < M && col < N) write_c_as<DT, EPI>(args, row * args.ldc + col, acc[i][j][r]);
+                const int dr = 32 * i + 8 * (r >> 2) + (r & 3);
+                if (dr < rows_left) base[dr * ldc + 32 * j] = convert_out<DT, EPI>(args, acc[i][j][r]);
             }
+            // One fragment at a time: keeps the scheduler from reading every accumulator
+            // out ahead of its stores.
+            __builtin_amdgcn_sched_barrier(0);
         }
+    }
 }
 
 // s_last: one int of LDS for the in-kernel split-K reduction's "last slice"
