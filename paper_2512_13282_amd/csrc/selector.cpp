@@ -160,7 +160,11 @@ bool select_plan(const Problem &p, Plan *out, int32_t forced_family, int32_t for
             const int32_t split = forced_split > 0 ? forced_split : s;
             Plan pl = evaluate(p, cfg, split, chip, forced_reduce);
             if (forced_split <= 0 && pl.split_k != split) continue;   // duplicate of a smaller split
-            if (!found || pl.t_total_us < best.t_total_us * (1.0 - 1e-9)) {
+            // Ties (memory-bound shapes, where every tile of one size moves the same
+            // bytes) go to the plan with the shorter compute time: the faster kernel.
+            const bool tie = found && std::abs(pl.t_total_us - best.t_total_us) <= 1e-9 * best.t_total_us;
+            if (!found || (!tie && pl.t_total_us < best.t_total_us) ||
+                (tie && pl.t_comp_us < best.t_comp_us * (1.0 - 1e-9))) {
                 best = pl;
                 found = true;
             }
