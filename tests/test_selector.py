@@ -232,3 +232,27 @@ def test_gemv_configs_only_for_one_row(dtype):
             plan(dtype, 1, 4096, 14336)                     # column-major-B kernel only
     finally:
         b.gemm_force_plan(dtype, b.GEMM_KERNEL_AUTO, -1, 0)
+
+
+@pytest.mark.parametrize("dtype", [I8, BF])
+def test_memory_bound_ties_go_to_the_faster_kernel(dtype):
+    # (M, K, N) = (2048, 256, 8192): every 256 x 256 config moves the same bytes, so the
+    # modelled totals tie; the choice must be the tied plan with the shortest compute time.
+    M, K, N = 2048, 256, 8192
+    p = plan(dtype, M, N, K)
+    assert p["model_t_mem_us"] > p["model_t_comp_us"]
+    try:
+        for cfg in range(64):
+            if b.gemm_force_plan(dtype, b.GEMM_KERNEL_AUTO, cfg, 0) != b.GEMM_OK:
+                break
+            try:
+                q = plan(dtype, M, N, K)
+            except b.GemmError:
+                continue
+            same_total = (abs(max(q["model_t_comp_us"], q["model_t_mem_us"]) -
+                              max(p["model_t_comp_us"], p["model_t_mem_us"])) < 1e-9 and
+                          q["split_k"] == p["split_k"])
+            if same_total:
+                assert q["model_t_comp_us"] >= p["model_t_comp_us"] - 1e-9, (q["name"], p["name"])
+    finally:
+        b.gemm_force_plan(dtype, b.GEMM_KERNEL_AUTO, -1, 0)
