@@ -69,6 +69,8 @@ def parse():
                     help="also time the GEMM over M, K, N in multiples of the 256 tile up to 8192, both "
                          "dtypes and B layouts (the paper's > 400-size sweep); details in "
                          "OUT_DIR/paper_sweep.jsonl, summary in the JSON line")
+    ap.add_argument("--sweep-set", choices=("all", "skinny"), default="all",
+                    help="workloads --sweep times: all of them, or only the skinny (M <= 64) ones")
     ap.add_argument("--out-dir", default="bench_out",
                     help="directory (relative to the repository root unless absolute) for the "
                          "per-point files of --sweep and --paper-sweep")
@@ -488,7 +490,7 @@ def main():
         from paper_2512_13282_amd import inputs
         os.makedirs(os.path.join(ROOT, args.out_dir), exist_ok=True)
         with open(os.path.join(ROOT, args.out_dir, "sweep.jsonl"), "w") as f:
-            for (dtype, M, K, N) in inputs.ALL_CONFIGS:
+            for (dtype, M, K, N) in (inputs.SKINNY if args.sweep_set == "skinny" else inputs.ALL_CONFIGS):
                 e = 1 if dtype == "int8" else 2
                 bbytes = K * N * e
                 copies = 1 if M >= 256 else max(1, int(np.ceil(512e6 / bbytes)) + 1)
