@@ -2154,18 +2154,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(KernelArgs a) {
     const int64_t total = a.M * a.N;
     const int64_t stride = int64_t(gridDim.x) * blockDim.x;
     for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total; idx += stride) {
-        // Up to sixteen slices' loads in flight at once, then summed in slice order:
-        // ((ws[0] + ws[1]) + ws[2]) + ..., the order of the in-kernel reduction.
-        sum_t s = sum_t(0);
-        for (int32_t p0 = 0; p0 < a.split_k; p0 += 16) {
-            sum_t v[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u)
-                v[u] = p0 + u < a.split_k ? ws[int64_t(p0 + u) * total + idx] : sum_t(0);
-#pragma unroll
-            for (int u = 0; u < 16; ++u)
-                if (p0 + u < a.split_k) s = (p0 + u == 0) ? v[u] : s + v[u];
-        }
+        sum_t s = ws[idx];
+        for (int32_t p = 1; p < a.split_k; ++p) s += ws[int64_t(p) * total + idx];
         const int64_t row = idx / a.N, col = idx % a.N;
         write_c<DT>(a, row * a.ldc + col, s);
     }
