@@ -418,8 +418,8 @@ def main():
         write_traffic(*args.traffic_from)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(GEMM shards by output tiles; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py times one GPU: the library has no multi-GPU path (a GEMM would shard by "
+              "output tiles, each GPU computing its own columns of C). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
