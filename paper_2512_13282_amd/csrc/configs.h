@@ -92,6 +92,10 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,     256, 256, 4, 2, 1, 5, 0.40, 0.45, 1, "ring_256x256_w8t_r5"},
     {FAM_RING,     256, 256, 2, 4, 1, 5, 0.40, 0.45, 1, "ring_256x256_w8_r5"},
     {FAM_RING,     256, 256, 2, 2, 1, 5, 0.38, 0.42, 1, "ring_256x256_w4_r5"},
+    {FAM_RING,     128, 256, 2, 2, 2, 3, 0.36, 0.34, 1, "ring_128x256_w4_r3"},
+    {FAM_RING,     256, 128, 2, 2, 2, 3, 0.36, 0.34, 1, "ring_256x128_w4_r3"},
+    {FAM_RING,     128, 256, 1, 4, 2, 3, 0.36, 0.34, 1, "ring_128x256_w4c_r3"},
+    {FAM_RING,     128, 256, 2, 4, 4, 3, 0.36, 0.34, 1, "ring_128x256_w8_r3"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

@@ -2234,6 +2234,10 @@ static hipError_t launch_config_bt(int32_t cfg, const KernelArgs &a, int64_t gri
         case 34: return launch_ring<DT, 256, 256, 4, 2, 2, 5>(a, grid, s);
         case 35: return launch_ring<DT, 256, 256, 2, 4, 2, 5>(a, grid, s);
         case 36: return launch_ring<DT, 256, 256, 2, 2, 1, 5>(a, grid, s);
+        case 37: return launch_ring<DT, 128, 256, 2, 2, 2, 3>(a, grid, s);
+        case 38: return launch_ring<DT, 256, 128, 2, 2, 2, 3>(a, grid, s);
+        case 39: return launch_ring<DT, 128, 256, 1, 4, 2, 3>(a, grid, s);
+        case 40: return launch_ring<DT, 128, 256, 2, 4, 4, 3>(a, grid, s);
         case 27:
             hipLaunchKernelGGL((gemv_bt_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
@@ -2268,7 +2272,8 @@ static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, 
             hipLaunchKernelGGL((gemm_stream_kernel<DT, 64, 3>), dim3(unsigned(grid)), dim3(256), 0, s, a);
             return hipGetLastError();
         case 16: case 17: case 18: case 19: case 20: case 21: case 22: case 23: case 24: case 25:
-        case 28: case 29: case 30: case 31: case 32: case 33: case 34: case 35: case 36:
+        case 28: case 29: case 30: case 31: case 32: case 33: case 34: case 35: case 36: case 37: case 38:
+        case 39: case 40:
             return launch_config_bt<DT>(cfg, a, grid, s);   // the ring kernels take either B layout
         case 26:
             hipLaunchKernelGGL((gemv_kernel<DT>), dim3(unsigned(grid)), dim3(256), 0, s, a);

@@ -17,7 +17,7 @@ import gpu_helpers as g
 
 pytestmark = pytest.mark.gpu
 I8, BF = g.I8, g.BF
-NUM_CONFIGS = 37
+NUM_CONFIGS = 41
 GENERIC_CONFIGS = (0, 1)
 GEMV_CONFIGS = (26, 27)      # M = 1 only: tests/test_gpu_gemv.py
 TILE_CONFIGS = [c for c in range(NUM_CONFIGS) if c not in GEMV_CONFIGS]
@@ -76,7 +76,7 @@ def test_every_config_matches_oracle(dtype, config, split, reduce):
             assert g.call(dtype, M, N, K, dA, lda, dB, ldb, dC, ldc) == b.GEMM_ERR_UNSUPPORTED
 
 
-@pytest.mark.parametrize("config", [0, 2, 3, 5, 6, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36])
+@pytest.mark.parametrize("config", [0, 2, 3, 5, 6, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36, 37, 38, 39, 40])
 def test_bf16_integer_valued_is_exact(config):
     """Integer-valued bf16 in [-8, 8]: the fp32 result is exact whatever the order."""
     M, N, K = 200, 264, 4096
@@ -266,7 +266,7 @@ def test_bf16_split_k_is_reproducible():
     g.check_bf16(A, B, c1)
 
 
-@pytest.mark.parametrize("config", [2, 3, 6, 0, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36])
+@pytest.mark.parametrize("config", [2, 3, 6, 0, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36, 37, 38, 39, 40])
 def test_int8_extremes_largest_k(config):
     """(-128)(-128) over K = 14336 is 234,881,024, the largest sum of the workload sweep."""
     g.force(I8, b.GEMM_KERNEL_AUTO, config, 0)

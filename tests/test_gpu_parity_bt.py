@@ -13,7 +13,7 @@ import gpu_helpers as g
 
 pytestmark = pytest.mark.gpu
 I8, BF = g.I8, g.BF
-BT_CONFIGS = (0, 1, 8, 9, 10, 11, 12, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36)
+BT_CONFIGS = (0, 1, 8, 9, 10, 11, 12, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36, 37, 38, 39, 40)
 GENERIC_CONFIGS = (0, 1)
 
 

@@ -64,8 +64,10 @@ def test_alignment_routes_to_generic(dtype):
 def test_workload_plans(dtype):
     d = DT[dtype]
     big = plan(d, 8192, 8192, 8192)
-    # the square 8192 problem fills the chip with 256 x 256 tiles and needs no split
-    assert big["bm"] == 256 and big["bn"] == 256 and big["split_k"] == 1
+    # the square 8192 problem fills the chip with large tiles (256 x 256, or two 128 x 256
+    # workgroups per compute unit) and needs no split
+    assert big["bm"] * big["bn"] >= 128 * 256 and big["bn"] == 256 and big["split_k"] == 1
+    assert big["grid"] >= 4 * 256
     for (_, M, K, N) in [c for c in inputs.ALL_CONFIGS if c[0] == dtype]:
         p = plan(d, M, N, K)
         check_invariants(p, d, M, N, K)
