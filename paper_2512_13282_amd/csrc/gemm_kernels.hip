@@ -1,30 +1,35 @@
 // gemm_kernels.hip -- gfx950 (CDNA4) MFMA GEMM kernels and their launcher.
 //
-// One kernel template serves both dtypes and every tile configuration of
-// configs.h.  Per workgroup (one output tile BM x BN, one K slice):
+// Kernel templates serve both dtypes and every tile configuration of configs.h.
+// Common to the tile kernels (one output tile BM x BN and one K slice per
+// workgroup):
 //
 //   * output-stationary: the accumulators of the whole tile stay in registers
-//     for every K stage (paper, Sec. 4.2.1); they start at zero, which replaces
-//     the paper's separate zeroing kernel;
-//   * K is walked in 128-byte stages (64 bf16 or 128 int8 elements).  Stage
-//     k+1 is fetched from global memory into registers while the MFMAs consume
-//     stage k from LDS, then written to the other LDS buffer: the double
-//     buffering of inputs (Sec. 4.2.1) with one barrier per stage;
-//   * LDS holds A as BM rows of 128 K-bytes and B transposed, BN rows of 128
-//     K-bytes, so that every MFMA operand fragment is one 16-byte LDS read.
-//     This is the on-the-fly layout transformation of Sec. 4.3: matrices stay
-//     row-major in memory and are re-tiled on the way into local memory.  B is
-//     row-major (K x N), so its K-contiguous fragments are produced by an
-//     in-register transpose of 8 x 8 (bf16) or 16 x 8 (int8) element blocks --
-//     the mirror image of the paper's in-core shuffle for column-major B
-//     (Sec. 4.3);
-//   * 16-byte chunks are XOR-swizzled within each 128-byte LDS row so that
-//     fragment reads and transposed writes spread over all banks;
+//     for the whole K slice (paper, Sec. 4.2.1); they start at zero, which
+//     replaces the paper's separate zeroing kernel;
+//   * K is walked in stages of 128 K-bytes (64 bf16 or 128 int8 elements), or
+//     in 64-byte slots for the ring kernels, with the next stage's operands in
+//     flight while the MFMAs consume the current one: the double buffering of
+//     inputs (Sec. 4.2.1), generalised to deeper rings;
+//   * LDS holds A as BM rows of K-bytes and B either as BN rows of K-bytes
+//     (column-major B, and the register-staged kernels, which transpose B in
+//     registers) or as K rows of BN elements read back with the LDS transpose
+//     reads, so every MFMA operand fragment is one 16-byte or two 8-byte LDS
+//     reads.  Matrices stay in their standard order in memory and are re-tiled
+//     on the way into local memory, as in Sec. 4.3;
+//   * 16-byte chunks are XOR-swizzled within LDS rows so that fragment reads
+//     and writes spread over all banks;
 //   * workgroup ids are remapped so that each XCD (workgroups are dealt
 //     round-robin to the 8 XCDs) runs a compact block of output tiles that
 //     shares A row-panels and B column-panels in its L2 -- the GPU analog of
 //     broadcasting A tiles along array rows and B tiles along columns
 //     (Sec. 4.2.1).
+//
+// Families: gemm_lds_kernel (DIRECT: global -> LDS buffer loads into two
+// stages), gemm_ring_kernel (RING: the same loads into a ring of 64-byte
+// slots), gemm_vec_kernel / gemm_tile_kernel (MACRO / GENERIC: loads through
+// registers), gemm_stream_kernel (narrow-M streaming), gemv_kernel and
+// gemv_bt_kernel (M = 1 on the vector ALUs), plus the split-K reduction.
 //
 // MFMA fragment layout used (32 x 32 output, 64 lanes): lane l supplies row
 // (l mod 32) of the A tile and column (l mod 32) of the B tile, each with 16
