@@ -306,6 +306,7 @@ int oracle_requant_i32(const int32_t *in, int64_t n, int shift, int bits, int32_
 uint16_t oracle_bf16_from_double(double x)
 {
     const uint16_t sign = signbit(x) ? 0x8000u : 0u;
+    if (isnan(x)) return (uint16_t)(sign | 0x7FC0u);   /* NaN stays NaN (the quiet NaN) */
     const double ax = fabs(x);
     if (ax == 0.0) return sign;
     int e;

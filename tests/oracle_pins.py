@@ -439,4 +439,14 @@ def pin_bf16_round_specials(o):
         assert got == want, (x, hex(got), hex(want))
 
 
+def pin_bf16_round_nan_inf(o):
+    """Infinities keep their sign; a NaN (either sign) rounds to a NaN: all-ones exponent,
+    non-zero significand (IEEE 754 rounding never turns a NaN into a number)."""
+    assert o.bf16_from_double(math.inf) == 0x7F80
+    assert o.bf16_from_double(-math.inf) == 0xFF80
+    for x in (math.nan, -math.nan, float(np.float32(np.nan))):
+        b = o.bf16_from_double(x)
+        assert (b & 0x7F80) == 0x7F80 and (b & 0x007F) != 0, hex(b)
+
+
 PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

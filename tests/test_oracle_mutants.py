@@ -84,6 +84,9 @@ MUTANTS = [
     ("bf16_round_no_subnormal_floor",
      "if (ulp_exp < -133) ulp_exp = -133;",
      "if (ulp_exp < -149) ulp_exp = -149;"),
+    ("bf16_round_nan_to_inf",
+     "if (isnan(x)) return (uint16_t)(sign | 0x7FC0u);",
+     "if (isnan(x)) return (uint16_t)(sign | 0x7F80u);"),
     ("freivalds_skip_last_row",
      "for (int64_t i = 0; i < M; ++i) {\n            __int128 lhs",
      "for (int64_t i = 0; i < M - 1; ++i) {\n            __int128 lhs"),
