@@ -36,7 +36,7 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (AMD published)
 HBM_GBS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2512_13282_amd", "csrc", "gemm_kernels.hip")
+KERNEL_DIR = os.path.join(ROOT, "paper_2512_13282_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 COPY_PROBE_BYTES = 512 * 1024 * 1024
 REQUANT_SHIFT = 14          # int8 -> int8 output: results / 2^14 (|C| <= 2^21 at K = 8192 for uniform int8)
@@ -80,7 +80,12 @@ def parse():
 
 
 def kernel_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    """Hash of the device sources (every .hip and .h of the library), in name order."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_DIR)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode() + b"\0" + open(os.path.join(KERNEL_DIR, name), "rb").read())
+    return h.hexdigest()
 
 
 def traffic_for(dtype: str, M: int, N: int, K: int, bt: bool = False):

@@ -2,12 +2,15 @@
 
     python -m paper_2512_13282_amd.build          # or build() from Python
 
-Host-only sources (the C ABI and the selector) compile with g++; the kernels
-compile with hipcc for gfx950; hipcc links the shared library.  Every call
+Host-only sources (the C ABI and the selector) compile with g++; the kernel
+translation units (one per kernel family, see csrc/families.h) compile with
+hipcc for gfx950, in parallel; hipcc links the shared library.  Every call
 recompiles.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
+import glob
 import os
 import shutil
 import subprocess
@@ -21,7 +24,7 @@ LIB = os.path.join(PKG, "libgemm_mi355x.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HOST_SOURCES = ["gemm_api.cpp", "selector.cpp"]
-DEVICE_SOURCES = ["gemm_kernels.hip", "mfma_probe.hip"]
+DEVICE_SOURCES = sorted(os.path.basename(p) for p in glob.glob(os.path.join(CSRC, "*.hip")))
 
 # Packed-fp32 instructions are disabled for all device code (the hipcc host
 # pass warns that it does not know the feature; that warning is harmless).
@@ -41,17 +44,20 @@ def _run(cmd: list[str]) -> None:
 def build(out: str = LIB, verbose: bool = False) -> str:
     tmp = tempfile.mkdtemp(prefix="gemm_build_")
     try:
-        objs = []
+        jobs = []
         for src in HOST_SOURCES:
-            obj = os.path.join(tmp, src + ".o")
-            _run(["g++", *HOST_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
-                  os.path.join(CSRC, src), "-o", obj])
-            objs.append(obj)
+            jobs.append(["g++", *HOST_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
+                         os.path.join(CSRC, src), "-o", os.path.join(tmp, src + ".o")])
         for src in DEVICE_SOURCES:
-            obj = os.path.join(tmp, src + ".o")
-            _run([HIPCC, *DEVICE_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
-                  os.path.join(CSRC, src), "-o", obj])
-            objs.append(obj)
+            jobs.append([HIPCC, *DEVICE_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
+                         os.path.join(CSRC, src), "-o", os.path.join(tmp, src + ".o")])
+        objs = [j[-1] for j in jobs]
+        # The slowest translation units (the ring and direct families) first, one compiler per core.
+        weight = lambda j: next((i for i, k in enumerate(("ring", "direct", "tile")) if k in j[-3]), 3)
+        jobs.sort(key=weight)
+        workers = max(1, min(len(jobs), os.cpu_count() or 1, 16))
+        with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(_run, jobs))
         _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", out + ".tmp"])
         os.replace(out + ".tmp", out)
         if verbose:

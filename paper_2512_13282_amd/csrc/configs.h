@@ -1,7 +1,8 @@
 // configs.h -- the tile configurations compiled into the library.
 //
 // One table, read by the host-side selector (selector.cpp) and by the launch
-// code (gemm_kernels.hip), which instantiates exactly these kernels.  Pure C++:
+// code (gemm_launch.hip and the launch_*.hip family units), which instantiates
+// exactly these kernels.  Pure C++:
 // no HIP headers, so the selector builds and tests on a machine without a GPU.
 //
 // Tiling levels (paper, Sec. 4.1: instruction tile r x s x t -> per-core kernel
@@ -95,7 +96,7 @@ constexpr TileConfig kConfigs[] = {
     {FAM_RING,     128, 256, 2, 2, 2, 3, 0.36, 0.34, 1, "ring_128x256_w4_r3"},
     {FAM_RING,     256, 128, 2, 2, 2, 3, 0.36, 0.34, 1, "ring_256x128_w4_r3"},
     {FAM_RING,     128, 256, 1, 4, 2, 3, 0.36, 0.34, 1, "ring_128x256_w4c_r3"},
-    {FAM_RING,     128, 256, 2, 4, 4, 3, 0.36, 0.34, 1, "ring_128x256_w8_r3"},
+    {FAM_RING,     128, 256, 2, 4, 2, 3, 0.36, 0.34, 1, "ring_128x256_w8_r3"},
 };
 constexpr int32_t kNumConfigs = int32_t(sizeof(kConfigs) / sizeof(kConfigs[0]));
 

@@ -2,7 +2,7 @@
 //
 // Validation happens here, on the host, before any HIP call; the plan comes
 // from the selector (cached per shape/alignment class); the launch goes
-// through launch_gemm (gemm_kernels.hip).
+// through launch_gemm (gemm_launch.hip).
 #include <stdint.h>
 #include <string.h>
 

@@ -1,0 +1,513 @@
+// gemm_common.h -- device helpers shared by every GEMM kernel family.
+//
+// Kernel templates serve both dtypes and every tile configuration of configs.h.
+// Common to the tile kernels (one output tile BM x BN and one K slice per
+// workgroup):
+//
+//   * output-stationary: the accumulators of the whole tile stay in registers
+//     for the whole K slice (paper, Sec. 4.2.1); they start at zero, which
+//     replaces the paper's separate zeroing kernel;
+//   * K is walked in stages of 128 K-bytes (64 bf16 or 128 int8 elements), or
+//     in 64-byte slots for the ring kernels, with the next stage's operands in
+//     flight while the MFMAs consume the current one: the double buffering of
+//     inputs (Sec. 4.2.1), generalised to deeper rings;
+//   * LDS holds A as BM rows of K-bytes and B either as BN rows of K-bytes
+//     (column-major B, and the register-staged kernels, which transpose B in
+//     registers) or as K rows of BN elements read back with the LDS transpose
+//     reads, so every MFMA operand fragment is one 16-byte or two 8-byte LDS
+//     reads.  Matrices stay in their standard order in memory and are re-tiled
+//     on the way into local memory, as in Sec. 4.3;
+//   * 16-byte chunks are XOR-swizzled within LDS rows so that fragment reads
+//     and writes spread over all banks;
+//   * workgroup ids are remapped so that each XCD (workgroups are dealt
+//     round-robin to the 8 XCDs) runs a compact block of output tiles that
+//     shares A row-panels and B column-panels in its L2 -- the GPU analog of
+//     broadcasting A tiles along array rows and B tiles along columns
+//     (Sec. 4.2.1).
+//
+// Families: gemm_lds_kernel (DIRECT: global -> LDS buffer loads into two
+// stages), gemm_ring_kernel (RING: the same loads into a ring of 64-byte
+// slots), gemm_vec_kernel / gemm_tile_kernel (MACRO / GENERIC: loads through
+// registers), gemm_stream_kernel (narrow-M streaming), gemv_kernel and
+// gemv_bt_kernel (M = 1 on the vector ALUs), plus the split-K reduction.
+//
+// MFMA fragment layout used (32 x 32 output, 64 lanes): lane l supplies row
+// (l mod 32) of the A tile and column (l mod 32) of the B tile, each with 16
+// bytes of K; lanes 0-31 and 32-63 hold two different 16-byte K halves.  Any
+// assignment of K positions is valid as long as A and B use the same one, and
+// both are read with the same (chunk, lane) mapping below.  Output register r
+// of lane l holds C[8*(r/4) + 4*(l/32) + (r mod 4)][l mod 32].
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "configs.h"
+#include "launch.h"
+
+namespace gemm {
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef int i32x16_t __attribute__((ext_vector_type(16)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+template <int DT> struct Types;
+template <> struct Types<DT_I8> {
+    using acc_vec = i32x16_t;
+    using out_t = int32_t;
+    static constexpr int E = 1;
+};
+template <> struct Types<DT_BF16> {
+    using acc_vec = f32x16_t;
+    using out_t = float;
+    static constexpr int E = 2;
+};
+
+template <int DT>
+__device__ __forceinline__ typename Types<DT>::acc_vec mfma32(u32x4_t a, u32x4_t b,
+                                                             typename Types<DT>::acc_vec c);
+template <>
+__device__ __forceinline__ i32x16_t mfma32<DT_I8>(u32x4_t a, u32x4_t b, i32x16_t c) {
+    return __builtin_amdgcn_mfma_i32_32x32x32_i8(__builtin_bit_cast(i32x4_t, a),
+                                                 __builtin_bit_cast(i32x4_t, b), c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x16_t mfma32<DT_BF16>(u32x4_t a, u32x4_t b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// Physical 16-byte chunk of logical chunk `c` in LDS row `row`.  Eight
+// consecutive rows (fragment reads) and rows eight apart (transposed B
+// writes) both land on eight distinct chunks.
+__device__ __forceinline__ int swz(int c, int row) { return c ^ ((row ^ (row >> 3)) & 7); }
+
+// Workgroup id -> (tile_m, tile_n, slice).  Consecutive hardware ids go to
+// different XCDs; the remap gives XCD x a contiguous range of logical ids, and
+// logical ids walk GROUP_M tile-rows column by column.
+__device__ __forceinline__ void map_tile(const KernelArgs &a, int &tm, int &tn, int &slice) {
+    const int total = int(gridDim.x);
+    const int hw = int(blockIdx.x);
+    const int per = total / 8, rem = total % 8;
+    const int xcd = hw % 8, local = hw / 8;
+    const int id = xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+    const int tiles = a.tiles_m * a.tiles_n;
+    slice = id / tiles;
+    const int t = id % tiles;
+    const int width = a.group_m * a.tiles_n;
+    const int group = t / width;
+    const int first_m = group * a.group_m;
+    const int gsize = (a.tiles_m - first_m) < a.group_m ? (a.tiles_m - first_m) : a.group_m;
+    const int in_group = t % width;
+    tm = first_m + in_group % gsize;
+    tn = in_group / gsize;
+}
+
+// Epilogue shared by every kernel: writes the accumulators of one wave (TM x
+// TN 32x32 MFMA tiles whose top-left output element is (r0, c0)) of the
+// BM x BN output tile (tm, tn) to C.
+//
+// With split-K each K slice stores its partial tile in the workspace
+// ([split][M][N]).  Then either a separate kernel sums the planes
+// (splitk_reduce_kernel), or, with args.reduce_in_kernel, every slice takes a
+// ticket from the tile's arrival counter and the workgroup that arrives last
+// sums the slices of the tile and writes C, then resets the counter to zero
+// for the next launch on the stream.  Both sum in the fixed slice order
+// 0, 1, ..., so fp32 results are identical run to run whichever slice finishes
+// last and whichever reduction runs.
+//
+// The slices of a tile run on different XCDs, whose L2 caches are not kept
+// coherent with each other for ordinary accesses.  Instead of device-scope
+// fences (which write back and invalidate the whole L2 of the XCD), the
+// partials are stored and loaded with device-scope (sc1) accesses, which go
+// to the device coherence point: each thread waits until its partial stores
+// are complete, the workgroup synchronises, and only then takes its ticket
+// (an atomic, itself coherent device-wide); the partial loads of the last
+// workgroup depend on the ticket and are issued after it.
+template <typename T>
+__device__ __forceinline__ void store_coherent(T *p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename T>
+__device__ __forceinline__ T load_coherent(const T *p) {
+    return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Output element idx (row * ldc + col, in output elements) of C from a result v of
+// the accumulator type, converted as the call's epilogue asks (launch.h).  int32
+// partial sums arrive as uint32 (they wrap modulo 2^32) and are read back as int32.
+__device__ __forceinline__ int32_t requant_nearest_even(int32_t v, int shift, int32_t lo, int32_t hi) {
+    const int64_t x = v;
+    int64_t q = x >> shift;                              // floor(x / 2^shift)
+    if (shift > 0) {
+        const int64_t r = x - (q << shift), half = int64_t(1) << (shift - 1);
+        if (r > half || (r == half && (q & 1))) ++q;
+    }
+    return int32_t(q < lo ? lo : (q > hi ? hi : q));
+}
+
+// fp32 -> bf16, round to nearest with ties to even.  A NaN keeps its upper half with
+// the quiet bit set (adding the rounding bias to a NaN could carry it into an
+// infinity, a zero or the sign); an infinity and a finite value past the largest
+// bf16 both land on the infinity.
+__device__ __forceinline__ uint16_t bf16_nearest_even(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return uint16_t((u >> 16) | 0x40u);
+    return uint16_t((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// Element type of C under epilogue EPI.
+template <int DT, int EPI> struct OutElem { using type = typename Types<DT>::out_t; };
+template <> struct OutElem<DT_I8, EPI_I8> { using type = int8_t; };
+template <> struct OutElem<DT_I8, EPI_I16> { using type = int16_t; };
+template <> struct OutElem<DT_BF16, EPI_BF16> { using type = uint16_t; };
+
+template <int DT, int EPI>
+__device__ __forceinline__ typename OutElem<DT, EPI>::type convert_out(const KernelArgs &a,
+                                                                         typename Types<DT>::out_t v) {
+    if constexpr (DT == DT_I8 && EPI == EPI_I8) return int8_t(requant_nearest_even(int32_t(v), a.shift, -128, 127));
+    else if constexpr (DT == DT_I8 && EPI == EPI_I16)
+        return int16_t(requant_nearest_even(int32_t(v), a.shift, -32768, 32767));
+    else if constexpr (DT == DT_BF16 && EPI == EPI_BF16) return bf16_nearest_even(float(v));
+    else return v;
+}
+
+template <int DT, int EPI, typename V>
+__device__ __forceinline__ void write_c_as(const KernelArgs &a, int64_t idx, V v) {
+    static_cast<typename OutElem<DT, EPI>::type *>(a.C)[idx] =
+        convert_out<DT, EPI>(a, typename Types<DT>::out_t(v));
+}
+
+template <int DT, typename V>
+__device__ __forceinline__ void write_c(const KernelArgs &a, int64_t idx, V v) {
+    if constexpr (DT == DT_I8) {
+        if (a.epilogue == EPI_I8) write_c_as<DT, EPI_I8>(a, idx, v);
+        else if (a.epilogue == EPI_I16) write_c_as<DT, EPI_I16>(a, idx, v);
+        else write_c_as<DT, EPI_NONE>(a, idx, v);
+    } else {
+        if (a.epilogue == EPI_BF16) write_c_as<DT, EPI_BF16>(a, idx, v);
+        else write_c_as<DT, EPI_NONE>(a, idx, v);
+    }
+}
+
+// A wave's output fragments straight into C with the epilogue EPI.  Lane l holds,
+// for fragment (i, j) and register r, row r0 + 4 (l / 32) + 32 i + 8 (r / 4) + r % 4
+// and column c0 + l % 32 + 32 j: one base pointer per lane plus a row offset that
+// is a constant times ldc, which the scalar unit forms.  The epilogue is a template
+// argument so that the loop bodies stay small enough to unroll fully: the
+// accumulators are then only indexed by constants and stay in registers (with a
+// run-time choice per element, the 256-register tiles of the 4-wave 256 x 256
+// int8 kernels went to scratch).
+template <int DT, int EPI, int TM, int TN>
+__device__ __forceinline__ void store_c_direct(const KernelArgs &args,
+                                               const typename Types<DT>::acc_vec (&acc)[TM][TN],
+                                               int64_t r0, int64_t c0, int lane) {
+    using o_t = typename OutElem<DT, EPI>::type;
+    const int64_t row0 = r0 + 4 * (lane >> 5);
+    const int64_t col = c0 + (lane & 31);
+    const int64_t rows_left = args.M - row0;
+    const int64_t ldc = args.ldc;
+    o_t *const base = static_cast<o_t *>(args.C) + row0 * ldc + col;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        if (col + 32 * j >= args.N) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int dr = 32 * i + 8 * (r >> 2) + (r & 3);
+                if (dr < rows_left) base[dr * ldc + 32 * j] = convert_out<DT, EPI>(args, acc[i][j][r]);
+            }
+            // One fragment at a time: keeps the scheduler from reading every accumulator
+            // out ahead of its stores.
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// s_last: one int of LDS for the in-kernel split-K reduction's "last slice"
+// broadcast; a kernel whose LDS is otherwise free at this point may lend it a word
+// of its operand buffers (all of its global -> LDS loads complete, all of its
+// fragment reads done).
+template <int DT, int BM, int BN, int TM, int TN>
+__device__ __forceinline__ void store_tile(const KernelArgs &args,
+                                           const typename Types<DT>::acc_vec (&acc)[TM][TN],
+                                           int tm, int tn, int slice, int64_t r0, int64_t c0, int lane,
+                                           int &s_last) {
+    using out_t = typename Types<DT>::out_t;
+    using sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;  // int32 wraps mod 2^32
+    const int frag_row = lane & 31, frag_half = lane >> 5;
+    const int64_t M = args.M, N = args.N;
+    const int64_t plane = M * N;
+    if (args.split_k == 1) {
+        // C itself, through the call's output conversion.
+        if constexpr (DT == DT_I8) {
+            if (args.epilogue == EPI_I8) store_c_direct<DT, EPI_I8>(args, acc, r0, c0, lane);
+            else if (args.epilogue == EPI_I16) store_c_direct<DT, EPI_I16>(args, acc, r0, c0, lane);
+            else store_c_direct<DT, EPI_NONE>(args, acc, r0, c0, lane);
+        } else {
+            if (args.epilogue == EPI_BF16) store_c_direct<DT, EPI_BF16>(args, acc, r0, c0, lane);
+            else store_c_direct<DT, EPI_NONE>(args, acc, r0, c0, lane);
+        }
+        return;
+    }
+    if (!args.reduce_in_kernel) {
+        // This slice's partial plane for the separate reduction.
+        out_t *out = static_cast<out_t *>(args.workspace) + int64_t(slice) * plane;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                    if (row < M && col < N) out[row * N + col] = acc[i][j][r];
+                }
+            }
+        return;
+    }
+
+    sum_t *ws = static_cast<sum_t *>(args.workspace);
+    {
+        sum_t *out = ws + int64_t(slice) * plane;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                    if (row < M && col < N) store_coherent(&out[row * N + col], sum_t(acc[i][j][r]));
+                }
+            }
+    }
+    const int tile = tm * args.tiles_n + tn;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's partial stores are complete
+    __syncthreads();                                   // ... and every thread's
+    if (threadIdx.x == 0) {
+        const unsigned ticket = __hip_atomic_fetch_add(&args.counters[tile], 1u, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+        s_last = ticket == unsigned(args.split_k - 1);
+    }
+    __syncthreads();
+    if (!s_last) return;
+
+    // Last slice of this tile: C = ((ws[0] + ws[1]) + ws[2]) + ... over the valid part of the
+    // tile, by all threads, consecutive columns per thread, with up to sixteen slices in flight.
+    const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+    const int rows = int(M - m0 < BM ? M - m0 : BM);
+    const int cols = int(N - n0 < BN ? N - n0 : BN);
+    const int split = args.split_k;
+    constexpr int V = 2;                               // columns per thread and pass
+    const int groups = (cols + V - 1) / V;
+    for (int q = int(threadIdx.x); q < rows * groups; q += int(blockDim.x)) {
+        const int rr = q / groups, cv = (q % groups) * V;
+        const int64_t base = (m0 + rr) * N + n0 + cv;
+        const int nv = cols - cv < V ? cols - cv : V;
+        sum_t s[V];
+        for (int p0 = 0; p0 < split; p0 += 16) {
+            sum_t v[16][V];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const sum_t *src = ws + int64_t(p0 + u < split ? p0 + u : 0) * plane + base;
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[u][e] = e < nv ? load_coherent(src + e) : sum_t(0);
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (p0 + u < split) {
+#pragma unroll
+                    for (int e = 0; e < V; ++e) s[e] = (p0 + u == 0) ? v[u][e] : s[e] + v[u][e];
+                }
+        }
+        const int64_t dst = (m0 + rr) * args.ldc + n0 + cv;
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+            if (e < nv) write_c<DT>(args, dst + e, s[e]);
+    }
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&args.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int DT, int BM, int BN, int WM, int WN, bool VEC>
+struct TileKernel {
+    static constexpr int THREADS = 64 * WM * WN;
+    static constexpr int E = Types<DT>::E;
+    static constexpr int VECE = 16 / E;          // elements per 16-byte chunk
+    static constexpr int BK = kStageKBytes / E;  // elements per stage
+    static constexpr int TM = BM / WM / 32;      // 32x32 MFMA tiles per wave along M
+    static constexpr int TN = BN / WN / 32;
+    static constexpr int A_CHUNKS = BM * 8 / THREADS;
+    // Vector B loader: one block = 8 columns x KPB k-rows, transposed into 8
+    // column pieces of KPB*E bytes (16 = whole chunk, 8 = half chunk).
+    static constexpr bool B_FULL = BN >= THREADS;
+    static constexpr int KPB = (B_FULL ? 16 : 8) / E;
+    static constexpr int OUTB = KPB * E;
+    static constexpr int B_BLOCKS = (BK / KPB) * (BN / 8) / THREADS;
+    static constexpr int ROWW = 16 / E == 8 ? 4 : 2;  // dwords per loaded B row piece
+    // Element-wise B loader: BN*8 chunks.
+    static constexpr int B_CHUNKS = BN * 8 / THREADS;
+
+    static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "wave tile must hold 32x32 MFMAs");
+    static_assert(A_CHUNKS >= 1 && A_CHUNKS * THREADS == BM * 8, "A stage must split evenly");
+    static_assert(!VEC || (B_BLOCKS >= 1 && B_BLOCKS * THREADS == (BK / KPB) * (BN / 8)),
+                  "B stage must split evenly");
+    static_assert(VEC || (B_CHUNKS >= 1 && B_CHUNKS * THREADS == BN * 8), "B chunks split evenly");
+};
+
+// ---------------------------------------------------------------------------
+// In-register transposes of a B block (row-major pieces -> K-contiguous
+// column pieces).  bf16: row piece = 8 columns (4 dwords, column c in dword
+// c/2, half c%2); int8: row piece = 8 columns (2 dwords, column c in dword
+// c/4, byte c%4).
+// ---------------------------------------------------------------------------
+template <int N>
+__device__ __forceinline__ unsigned bf16_col_dword(const u32x4_t (&rows)[N], int base, int c, int j) {
+    const unsigned lo = rows[base + 2 * j][c >> 1], hi = rows[base + 2 * j + 1][c >> 1];
+    return (c & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+}
+
+template <int N>
+__device__ __forceinline__ unsigned i8_col_dword(const u32x2_t (&rows)[N], int base, int c, int j) {
+    const int sh = 8 * (c & 3);
+    const unsigned b0 = (rows[base + 4 * j + 0][c >> 2] >> sh) & 0xFFu;
+    const unsigned b1 = (rows[base + 4 * j + 1][c >> 2] >> sh) & 0xFFu;
+    const unsigned b2 = (rows[base + 4 * j + 2][c >> 2] >> sh) & 0xFFu;
+    const unsigned b3 = (rows[base + 4 * j + 3][c >> 2] >> sh) & 0xFFu;
+    return b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+}
+
+
+// v_perm_b32 byte select: selector byte values 0-3 pick bytes of the SECOND
+// operand, 4-7 bytes of the FIRST.
+__device__ __forceinline__ unsigned perm(unsigned hi, unsigned lo, unsigned sel) {
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+// bf16 block: rows[base .. base+KPB) are row pieces of 8 columns (column c in
+// dword c/2, half c%2).  col[c][j] = (row 2j, row 2j+1) of column c.
+template <int KPB, int N>
+__device__ __forceinline__ void bf16_transpose(const u32x4_t (&rows)[N], int base, unsigned (&col)[8][KPB / 2]) {
+#pragma unroll
+    for (int j = 0; j < KPB / 2; ++j)
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            col[c][j] = perm(rows[base + 2 * j + 1][c >> 1], rows[base + 2 * j][c >> 1],
+                             (c & 1) ? 0x07060302u : 0x05040100u);
+}
+
+// int8 block: row pieces of 8 columns (column c in dword c/4, byte c%4).
+// col[c][j] = bytes (row 4j, 4j+1, 4j+2, 4j+3) of column c: pairs of rows are
+// interleaved bytewise first, then pairs of pairs halfword-wise.
+template <int KPB, int N>
+__device__ __forceinline__ void i8_transpose(const u32x2_t (&rows)[N], int base, unsigned (&col)[8][KPB / 4]) {
+#pragma unroll
+    for (int j = 0; j < KPB / 4; ++j)
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+            const unsigned r0 = rows[base + 4 * j + 0][d], r1 = rows[base + 4 * j + 1][d];
+            const unsigned r2 = rows[base + 4 * j + 2][d], r3 = rows[base + 4 * j + 3][d];
+            const unsigned lo01 = perm(r1, r0, 0x05010400u), hi01 = perm(r1, r0, 0x07030602u);
+            const unsigned lo23 = perm(r3, r2, 0x05010400u), hi23 = perm(r3, r2, 0x07030602u);
+            col[4 * d + 0][j] = perm(lo23, lo01, 0x05040100u);
+            col[4 * d + 1][j] = perm(lo23, lo01, 0x07060302u);
+            col[4 * d + 2][j] = perm(hi23, hi01, 0x05040100u);
+            col[4 * d + 3][j] = perm(hi23, hi01, 0x07060302u);
+        }
+}
+
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
+
+constexpr int kBufferFlags = 0x00020000;   // raw untyped dword access (gfx9 family descriptor word 3)
+constexpr uint32_t kOOB = 0x80000000u;     // offset past any resource used here -> load returns 0
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint8_t *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(base), (short)0, (int)bytes, kBufferFlags);
+}
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+
+template <int DT> __device__ __forceinline__ int bswz(int k);
+template <> __device__ __forceinline__ int bswz<DT_BF16>(int k) {
+    const int m = k & 3;
+    return (m << 2) ^ ((m >> 1) << 1);          // 0, 4, 10, 14
+}
+template <> __device__ __forceinline__ int bswz<DT_I8>(int k) {
+    const int m = k & 7;
+    return (m << 1) | (m >> 2);                 // 0, 2, 4, 6, 9, 11, 13, 15
+}
+
+template <int DT> __device__ __forceinline__ u32x2_t lds_read_tr(const uint8_t *p);
+template <> __device__ __forceinline__ u32x2_t lds_read_tr<DT_BF16>(const uint8_t *p) {
+    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                                           (LDS_AS bf16x4_t *)(const_cast<uint8_t *>(p))));
+}
+template <> __device__ __forceinline__ u32x2_t lds_read_tr<DT_I8>(const uint8_t *p) {
+    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                                           (LDS_AS i32x2_t *)(const_cast<uint8_t *>(p))));
+}
+
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, uint8_t *lds_wave_base, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LDS_AS void *)lds_wave_base, 16, int(voff), 0, 0, 0);
+}
+
+__device__ __forceinline__ int ring_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+
+// Buffer resource as four dwords (base, stride 0, size in bytes, raw-access flags)
+// for the inline-assembly load below.
+__device__ __forceinline__ i32x4_t ring_rsrc(const uint8_t *base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return i32x4_t{int(uint32_t(a)), int(uint32_t(a >> 32) & 0xffffu), int(bytes), kBufferFlags};
+}
+
+// One wave-wide 16-byte-per-lane global -> LDS load: lane l's 16 bytes from
+// rsrc + voff land at LDS byte lds + 16 l.  Written as inline assembly so that
+// the compiler does not tie the LDS reads that follow to these writes (it cannot
+// tell the ring buffers apart and would wait for every load in flight before each
+// read); completion is tracked by the explicit vmcnt waits of the ring instead,
+// and nothing else in the kernel accesses the ring.
+// The LDS address goes in M0, which the "{m0}" operand has the compiler load.
+__device__ __forceinline__ void ring_load16(i32x4_t rsrc, uint32_t lds, uint32_t voff) {
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" :: "v"(voff), "s"(rsrc), "{m0}"(lds) : "memory");
+}
+
+// The same with 4 bytes per lane: lane l's dword lands at LDS byte lds + 4 l.
+__device__ __forceinline__ void ring_load4(i32x4_t rsrc, uint32_t lds, uint32_t voff) {
+    asm volatile("buffer_load_dword %0, %1, 0 offen lds" :: "v"(voff), "s"(rsrc), "{m0}"(lds) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t *p) {
+    return uint32_t(reinterpret_cast<uintptr_t>((LDS_AS const void *)p));
+}
+
+template <int VMCNT>
+__device__ __forceinline__ void ring_barrier() {
+    static_assert(VMCNT >= 0 && VMCNT < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(VMCNT) : "memory");
+}
+
+__device__ __forceinline__ void phase_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+__device__ __forceinline__ void stage_barrier() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+}  // namespace gemm

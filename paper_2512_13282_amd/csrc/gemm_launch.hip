@@ -1,0 +1,155 @@
+// gemm_launch.hip -- routes a plan to its kernel family and owns the split-K
+// workspaces.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "configs.h"
+#include "families.h"
+#include "launch.h"
+
+namespace gemm {
+
+// Configuration index -> the translation unit that compiles it.  The streaming
+// narrow-M kernels (configurations 14 and 15) are SKINNY by purpose but live
+// with the other small-shape kernels.
+template <int DT>
+static hipError_t launch_config(int32_t cfg, const KernelArgs &a, int64_t grid, hipStream_t s) {
+    if (cfg < 0 || cfg >= kNumConfigs) return hipErrorInvalidValue;
+    switch (kConfigs[cfg].family) {
+        case FAM_GENERIC:
+        case FAM_MACRO: return launch_tile_family<DT>(cfg, a, grid, s);
+        case FAM_SKINNY:
+            return (cfg == 14 || cfg == 15) ? launch_small_family<DT>(cfg, a, grid, s)
+                                            : launch_tile_family<DT>(cfg, a, grid, s);
+        case FAM_DIRECT: return launch_direct_family<DT>(cfg, a, grid, s);
+        case FAM_RING:
+            return a.b_trans ? launch_ring_family<DT, true>(cfg, a, grid, s)
+                             : launch_ring_family<DT, false>(cfg, a, grid, s);
+        case FAM_GEMV: return launch_small_family<DT>(cfg, a, grid, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+__global__ __launch_bounds__(256) void zero_u32_kernel(uint32_t *__restrict__ p, int64_t n) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0u;
+}
+
+// Split-K workspace, one per (device, stream): the partial planes and the
+// per-tile arrival counters.  Kept for the life of the process and grown on
+// demand, so a split-K call costs no allocation and no extra launch.  Every
+// buffer is allocated, zeroed (counters) and released in stream order on the
+// stream that uses it, so work still queued with an old buffer is unaffected
+// by its replacement.  Launches on one stream run in order and each launch
+// leaves every counter it touched at zero, which is what makes the counters
+// reusable; separate streams get separate workspaces.
+namespace {
+struct Workspace {
+    void *partials = nullptr;
+    size_t partial_bytes = 0;
+    uint32_t *counters = nullptr;
+    int64_t counter_cap = 0;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, uintptr_t>, Workspace> g_ws;
+
+size_t grow(size_t need, size_t have, size_t quantum) {
+    size_t n = need > 2 * have ? need : 2 * have;
+    return (n + quantum - 1) / quantum * quantum;
+}
+}  // namespace
+
+static int acquire_workspace(hipStream_t stream, size_t partial_bytes, int64_t tiles, void **partials,
+                             uint32_t **counters) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return LAUNCH_HIP_ERROR;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    Workspace &w = g_ws[{dev, reinterpret_cast<uintptr_t>(stream)}];
+    if (w.partial_bytes < partial_bytes) {
+        if (w.partials != nullptr && hipFreeAsync(w.partials, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
+        w.partials = nullptr;
+        const size_t bytes = grow(partial_bytes, w.partial_bytes, size_t(1) << 20);
+        w.partial_bytes = 0;
+        if (hipMallocAsync(&w.partials, bytes, stream) != hipSuccess || w.partials == nullptr) {
+            (void)hipGetLastError();
+            w.partials = nullptr;
+            return LAUNCH_NO_MEMORY;
+        }
+        w.partial_bytes = bytes;
+    }
+    if (w.counter_cap < tiles) {
+        if (w.counters != nullptr && hipFreeAsync(w.counters, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
+        w.counters = nullptr;
+        const int64_t cap = int64_t(grow(size_t(tiles), size_t(w.counter_cap), 4096));
+        w.counter_cap = 0;
+        void *p = nullptr;
+        if (hipMallocAsync(&p, size_t(cap) * 4, stream) != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return LAUNCH_NO_MEMORY;
+        }
+        int64_t blocks = (cap + 255) / 256;
+        if (blocks > 1024) blocks = 1024;
+        hipLaunchKernelGGL(zero_u32_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream,
+                           static_cast<uint32_t *>(p), cap);
+        if (hipGetLastError() != hipSuccess) {
+            (void)hipFreeAsync(p, stream);
+            return LAUNCH_HIP_ERROR;
+        }
+        w.counters = static_cast<uint32_t *>(p);
+        w.counter_cap = cap;
+    }
+    *partials = w.partials;
+    *counters = w.counters;
+    return LAUNCH_OK;
+}
+
+int release_workspaces() {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return LAUNCH_HIP_ERROR;
+    int rc = LAUNCH_OK;
+    for (auto &kv : g_ws) {
+        Workspace &w = kv.second;
+        if (w.partials == nullptr && w.counters == nullptr) continue;
+        if (hipSetDevice(kv.first.first) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+            rc = LAUNCH_HIP_ERROR;
+            continue;
+        }
+        if (w.partials != nullptr && hipFree(w.partials) != hipSuccess) rc = LAUNCH_HIP_ERROR;
+        if (w.counters != nullptr && hipFree(w.counters) != hipSuccess) rc = LAUNCH_HIP_ERROR;
+        w = Workspace{};
+    }
+    g_ws.clear();
+    if (hipSetDevice(cur) != hipSuccess) rc = LAUNCH_HIP_ERROR;
+    return rc;
+}
+
+int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr) {
+    hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+    KernelArgs args = a;
+    args.workspace = nullptr;
+    args.counters = nullptr;
+    if (args.split_k > 1) {
+        const size_t bytes = size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
+        const int64_t tiles = args.reduce_in_kernel ? int64_t(args.tiles_m) * args.tiles_n : 0;
+        const int rc = acquire_workspace(stream, bytes, tiles, &args.workspace, &args.counters);
+        if (rc != LAUNCH_OK) return rc;
+    }
+    hipError_t e = args.dtype == DT_I8 ? launch_config<DT_I8>(cfg, args, grid, stream)
+                                       : launch_config<DT_BF16>(cfg, args, grid, stream);
+    if (e == hipSuccess && args.split_k > 1 && !args.reduce_in_kernel) {
+        const int64_t total = args.M * args.N;
+        int64_t blocks = (total + 255) / 256;
+        if (blocks > 8192) blocks = 8192;
+        // unsigned adds: int32 partials wrap modulo 2^32, defined
+        e = args.dtype == DT_I8 ? launch_splitk_reduce<DT_I8>(args, blocks, stream)
+                                : launch_splitk_reduce<DT_BF16>(args, blocks, stream);
+    }
+    return e == hipSuccess ? LAUNCH_OK : LAUNCH_HIP_ERROR;
+}
+
+}  // namespace gemm

@@ -19,10 +19,12 @@ DTYPES = ("int8", "bf16")
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
-    """Round finite float32 values to bf16 (nearest, ties to even); uint16 bits out."""
+    """Round float32 values to bf16 (nearest, ties to even); uint16 bits out.  Infinities
+    keep their sign; a NaN stays a NaN (its upper half with the quiet bit set)."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    u = u + 0x7FFF + ((u >> 16) & 1)
-    return (u >> 16).astype(np.uint16)
+    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    nan = (u & 0x7FFFFFFF) > 0x7F800000
+    return np.where(nan, (u >> 16) | 0x40, r).astype(np.uint16)
 
 
 def f32_from_bf16_bits(b: np.ndarray) -> np.ndarray:

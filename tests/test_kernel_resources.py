@@ -36,12 +36,24 @@ def kernels(tmp_path_factory):
         pytest.skip("library not built or LLVM tools missing")
     objcopy, bundler, readelf = tools
     d = tmp_path_factory.mktemp("codeobj")
-    fat, co = str(d / "fatbin.bin"), str(d / "gfx950.co")
+    fat = str(d / "fatbin.bin")
     subprocess.run([objcopy, "--dump-section", f".hip_fatbin={fat}", LIB, str(d / "stripped.so")],
                    check=True, capture_output=True)
-    subprocess.run([bundler, "--unbundle", "--type=o", f"--targets={TARGET}", f"--input={fat}",
-                    f"--output={co}"], check=True, capture_output=True)
-    notes = subprocess.run([readelf, "--notes", co], check=True, capture_output=True, text=True).stdout
+    # One offload bundle per translation unit, back to back in the section.
+    data = open(fat, "rb").read()
+    magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    starts, i = [], data.find(magic)
+    while i >= 0:
+        starts.append(i)
+        i = data.find(magic, i + 1)
+    notes = ""
+    for n, (a, b) in enumerate(zip(starts, starts[1:] + [len(data)])):
+        part, co = str(d / f"bundle{n}.bin"), str(d / f"gfx950_{n}.co")
+        with open(part, "wb") as f:
+            f.write(data[a:b])
+        subprocess.run([bundler, "--unbundle", "--type=o", f"--targets={TARGET}", f"--input={part}",
+                        f"--output={co}"], check=True, capture_output=True)
+        notes += subprocess.run([readelf, "--notes", co], check=True, capture_output=True, text=True).stdout
     out, cur = {}, None
     for line in notes.splitlines():
         m = re.match(r"\s*(?:- )?\.(\w+):\s+(\S+)", line)
@@ -91,3 +103,51 @@ def test_8192_plan_kernels_use_no_scratch(kernels):
 def test_lds_within_limit(kernels):
     for n, k in _gemm(kernels).items():
         assert int(k["group_segment_fixed_size"]) <= LDS_LIMIT, n
+
+
+def _configs():
+    """The tile configuration table, parsed from configs.h: one dict per row, in index order."""
+    src = open(os.path.join(ROOT, "paper_2512_13282_amd", "csrc", "configs.h")).read()
+    rows = re.findall(r'\{(FAM_\w+),\s*(\d+),\s*(\d+),\s*(\d+),\s*(\d+),\s*(\d+),\s*(\d+),\s*[\d.]+,\s*[\d.]+,'
+                      r'\s*(\d),\s*"(\w+)"\}', src)
+    keys = ("family", "bm", "bn", "wm", "wn", "occupancy", "stages", "col_major_b", "name")
+    return [dict(zip(keys, (r[0], *map(int, r[1:8]), r[8]))) for r in rows]
+
+
+def _config_kernels(cfg, index, kernels):
+    """Kernel instances (metadata dicts) that run configuration `cfg` (both dtypes, both B layouts)."""
+    f, bm, bn, wm, wn, st = cfg["family"], cfg["bm"], cfg["bn"], cfg["wm"], cfg["wn"], cfg["stages"]
+    geo = rf"ELi{bm}ELi{bn}ELi{wm}ELi{wn}E"
+    if f == "FAM_GENERIC":
+        pat = rf"gemm_tile_kernelILi[01]{geo}Lb0E"
+    elif f in ("FAM_MACRO", "FAM_SKINNY") and index not in (14, 15):
+        pat = rf"gemm_vec_kernelILi[01]{geo}"
+    elif index in (14, 15):
+        pat = rf"gemm_stream_kernelILi[01]ELi{bm}ELi{st}E"
+    elif index == 13:
+        pat = r"gemm_pingpong_kernel"
+    elif f == "FAM_DIRECT":
+        pat = rf"gemm_lds_kernelILi[01]{geo}Li\d+ELb[01]E"
+    elif f == "FAM_RING":
+        pat = rf"gemm_ring_kernelILi[01]{geo}Li\d+ELb[01]ELi{st}E"
+    else:
+        pat = r"gemv_bt_kernel" if cfg["col_major_b"] else r"gemv_kernel"
+    return {n: k for n, k in _gemm(kernels).items() if re.search(pat, n)}
+
+
+def test_config_occupancy_fits_the_cu(kernels):
+    """`occupancy` (workgroups resident per CU, used by the selector's wave-quantization model)
+    must be what the built kernels allow: occupancy x LDS within the CU's 160 KiB, and
+    occupancy x waves per SIMD x registers per wave within a SIMD's 512 registers per lane."""
+    cfgs = _configs()
+    assert len(cfgs) >= 41
+    for i, c in enumerate(cfgs):
+        ks = _config_kernels(c, i, kernels)
+        assert ks, (i, c["name"])
+        waves_per_simd = -(-c["wm"] * c["wn"] // 4) if c["family"] != "FAM_GEMV" else 1
+        for n, k in ks.items():
+            lds = int(k["group_segment_fixed_size"])
+            assert c["occupancy"] * lds <= LDS_LIMIT, (c["name"], n, lds)
+            regs = int(k.get("vgpr_count", 0)) + int(k.get("agpr_count", 0))
+            regs = -(-regs // 8) * 8
+            assert c["occupancy"] * waves_per_simd * regs <= 512, (c["name"], n, regs)
