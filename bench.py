@@ -1,24 +1,31 @@
 #!/usr/bin/env python3
 """Throughput of the MI355X GEMM library on the paper-shaped workload sweep.
 
-Default run (one GPU): the int8 -> int32 GEMM at M = N = K = 8192 (headline
-`value`, TOPS) and the bf16 -> fp32 GEMM at the same size (the `bf16` object),
-inputs resident in HBM, W untimed warm-up launches, then K timed launches
-bracketed by device synchronisation.  Prints ONE JSON line on stdout with a
-roofline object for the dominant kernel (HIP events on the launch stream) and
-the CPU oracle timed on a bounded sample of the same workload.
+Default run (one GPU), in this order:
 
-    python bench.py [--steps K] [--warmup W] [--size S] [--sweep]
+1. `configs`: every other workload of the sweep (int8 256^3, bf16 1024^3, the
+   2048^3 / 4096^3 squares, the three rectangles, the twelve skinny shapes),
+   each timed with HIP events on the launch stream under a labelled protocol
+   (cold for the cache-sized and the memory-bound shapes, warm otherwise), with
+   its plan, roofline fraction and sampled oracle rows;
+2. the headline: the int8 -> int32 GEMM at M = N = K = 8192 (`value`, TOPS) and
+   the bf16 -> fp32 GEMM at the same size (the `bf16` object), inputs resident
+   in HBM, W untimed warm-up launches, then K timed launches bracketed by device
+   synchronisation; each with the CPU oracle timed on a bounded sample of the
+   same workload (`cpu_baseline`) and the timed output compared with every
+   oracle row that sample computed (`parity_full`);
+3. the same two GEMMs with B stored column-major, and the sustained MFMA
+   ceiling of the chip.
+
+Prints ONE JSON line on stdout with a roofline object for the dominant kernel.
+
+    python bench.py [--steps K] [--warmup W] [--size S] [--no-configs] [--sweep]
+    python bench.py --workload int8:2048x2048x2048 --steps 50   # one workload (profiling)
 
 `--paper-sweep` times the GEMM over every (M, K, N) in multiples of the 256 tile
 up to 8192 (512 points per dtype and B layout).  `--reduced` also times the 8192^3
-GEMMs with narrowed outputs (int8 -> int8, bf16 -> bf16).
-
-`--sweep` also times every workload of the sweep (one JSON row each, on
-stderr and in OUT_DIR/sweep.jsonl); memory-bound shapes there rotate
-through enough copies of B to defeat the 256 MB last-level cache.  The same
-two 8192^3 GEMMs with B stored column-major (the *_bt entry points) are timed
-too and reported in the `column_major_b` object (`--no-bt` skips them).
+GEMMs with narrowed outputs (int8 -> int8, bf16 -> bf16).  `--sweep` writes one
+row per workload to OUT_DIR/sweep.jsonl.
 """
 from __future__ import annotations
 
@@ -76,6 +83,14 @@ def parse():
                          "per-point files of --sweep and --paper-sweep")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 512 MiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload table (every other workload of the sweep, timed before "
+                         "the headline)")
+    ap.add_argument("--config-steps", type=int, default=50, help="timed launches per workload of the table")
+    ap.add_argument("--config-warmup", type=int, default=20, help="untimed launches per workload of the table")
+    ap.add_argument("--workload", default=None, metavar="DTYPE:MxKxN",
+                    help="time only this workload (e.g. int8:2048x2048x2048) with --steps/--warmup and print "
+                         "one JSON line (for profiling one kernel)")
     return ap.parse_args()
 
 
@@ -173,6 +188,32 @@ def time_workload(w: Workload, steps: int, warmup: int):
     return wall * 1e3 / steps, float(np.mean(kernel_ms)), float(np.min(kernel_ms))
 
 
+FLUSH_BYTES = 512 * 1024 * 1024      # twice the last-level cache
+
+
+def time_workload_flushed(w: Workload, steps: int, warmup: int):
+    """Cold-cache timing for operands that fit in the caches: before every launch a 512 MiB
+    scratch buffer is written (evicting A, B and C from the L2s and the 256 MB last-level
+    cache), then the launch alone is timed with HIP events on the launch stream."""
+    import torch
+    scratch = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    for _ in range(warmup):
+        w.launch()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for i in range(steps):
+        scratch.fill_(float(i))
+        starts[i].record(w.stream)
+        w.launch()
+        ends[i].record(w.stream)
+    torch.cuda.synchronize()
+    kernel_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    del scratch
+    k_avg = float(np.mean(kernel_ms))
+    return k_avg, k_avg, float(np.min(kernel_ms))
+
+
 def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
     ops = 2.0 * w.M * w.N * w.K
     e = 1 if w.dtype == "int8" else 2
@@ -188,7 +229,8 @@ def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
         roof = {"bound": "hbm", "achieved": round(ach_gbs, 1), "peak": HBM_GBS, "unit": "GB/s",
                 "frac": round(ach_gbs / HBM_GBS, 4), "traffic": traffic}
     else:
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK[w.dtype], "unit": "TFLOP/s",
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK[w.dtype],
+                "unit": "TOPS" if w.dtype == "int8" else "TFLOP/s",
                 "frac": round(achieved / PEAK[w.dtype], 4), "traffic": traffic}
     return {
         "value": round(value, 2), "unit": "TOPS" if w.dtype == "int8" else "TFLOP/s",
@@ -225,6 +267,69 @@ def parity_sample(w: Workload, rows):
     return bool(err <= 1e-5)
 
 
+def parity_full(w: Workload):
+    """The timed output against the oracle rows cpu_baseline computed (all M rows when the
+    oracle finished the whole product): int8 element for element, bf16 by the normalized
+    error.  Returns None when no oracle rows are held."""
+    held = getattr(w, "oracle_rows", None)
+    if held is None:
+        return None
+    rows, out = held
+    C = w.dC[:rows].cpu().numpy()
+    if w.dtype == "int8":
+        ref, ovf = out
+        bad = int(np.count_nonzero(C != ref))
+        return {"rows_compared": rows, "of_rows": w.M, "mismatches": bad, "overflows": int(ovf),
+                "ok": bool(bad == 0 and ovf == 0), "rule": "bit-exact"}
+    from oracle import oracle
+    from paper_2512_13282_amd import inputs
+    err = oracle.normalized_error(C, out, w.K, float(np.abs(inputs.f32_from_bf16_bits(w.A_host)).max()),
+                                  float(np.abs(inputs.f32_from_bf16_bits(w.B_host)).max()))
+    return {"rows_compared": rows, "of_rows": w.M, "normalized_error": float(err), "ok": bool(err <= 1e-5),
+            "rule": "max|C - C_ref| / (K max|A| max|B|) <= 1e-5"}
+
+
+def config_table(skip, steps: int, warmup: int):
+    """Every workload of the sweep (inputs.ALL_CONFIGS) except those in `skip`, timed with
+    HIP events on the launch stream.  Shapes whose operands fit in the caches (int8 256^3,
+    bf16 1024^3) are timed cold, one launch at a time after a 512 MiB flush; the skinny
+    (memory-bound) shapes rotate through enough copies of B that more than 512 MB is read
+    between reuses of a copy; the rest are timed warm, back to back.  Each row carries its
+    protocol, plan, roofline fraction and a parity check of sampled output rows."""
+    import torch
+    from paper_2512_13282_amd import inputs
+    rows = []
+    for (dtype, M, K, N) in inputs.ALL_CONFIGS:
+        if (dtype, M, K, N) in skip:
+            continue
+        e = 1 if dtype == "int8" else 2
+        skinny = M < 256
+        copies = max(1, int(np.ceil(512e6 / (K * N * e))) + 1) if skinny else 1
+        w = Workload(dtype, M, N, K, copies=copies)
+        if (dtype, M, K, N) in inputs.SMALL:
+            ms, kavg, kmin = time_workload_flushed(w, steps, warmup)
+            proto = "cold: 512 MiB flush before each launch, launches timed one by one"
+        else:
+            ms, kavg, kmin = time_workload(w, steps, warmup)
+            proto = (f"cold: back to back, B rotated over {copies} copies (> 512 MB between reuses)"
+                     if skinny else "warm: back to back, operands resident")
+        r = summarize(w, ms, kavg, kmin)
+        ops = 2.0 * M * N * K
+        row = {"dtype": dtype, "M": M, "K": K, "N": N, "protocol": proto, "plan": r["plan"],
+               "split_k": r["split_k"], "kernel_us": round(kavg * 1e3, 2),
+               "value": round(ops / (kavg * 1e-3) / 1e12, 2), "unit": r["unit"],
+               "pct_dense_peak": round(100.0 * ops / (kavg * 1e-3) / 1e12 / PEAK[dtype], 2),
+               "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac")},
+               "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))}
+        rows.append(row)
+        print(f"[configs] {dtype:4s} M={M:5d} K={K:6d} N={N:6d} {row['kernel_us']:9.1f} us {row['value']:9.2f} "
+              f"{row['unit']:7s} {row['roofline']['bound']} frac={row['roofline']['frac']:.3f} plan={row['plan']} "
+              f"x{row['split_k']} ok={row['parity_sample_ok']}", file=sys.stderr, flush=True)
+        del w
+        torch.cuda.empty_cache()
+    return rows
+
+
 def cpu_baseline(w: Workload, seconds: float):
     """The oracle (as is) on the first rows of the same workload, sized to ~`seconds`."""
     from oracle import oracle
@@ -241,8 +346,9 @@ def cpu_baseline(w: Workload, seconds: float):
     rows = int(max(probe, min(w.M, probe * seconds / max(t_probe, 1e-6))))
     rows = max(threads, (rows // threads) * threads) if rows >= threads else rows
     t0 = time.perf_counter()
-    fn(np.ascontiguousarray(w.A_host[:rows]), w.B_host, nthreads=threads)
+    out = fn(np.ascontiguousarray(w.A_host[:rows]), w.B_host, nthreads=threads)
     t = time.perf_counter() - t0
+    w.oracle_rows = (rows, out)          # kept for the full comparison of the timed output
     ops = 2.0 * rows * w.N * w.K
     cpu = "unknown"
     try:
@@ -435,15 +541,33 @@ def main():
             if binding.gemm_force_plan(d, binding.GEMM_KERNEL_AUTO, args.config, 0) != 0:
                 sys.exit(f"cannot force config {args.config}")
 
+    if args.workload:
+        dtype, shape = args.workload.split(":")
+        M, K, N = (int(x) for x in shape.split("x"))
+        w = Workload(dtype, M, N, K)
+        ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+        r = summarize(w, ms, kavg, kmin)
+        r.update({"workload": args.workload, "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))})
+        print(json.dumps(r), flush=True)
+        return
+
     S = args.size
+    from paper_2512_13282_amd import inputs
+    heads = [(d, S, S, S) for d in (["int8", "bf16"] if args.only is None else [args.only])]
+    # The per-workload table runs first: besides its own figures, it brings the chip to the
+    # clock it holds under sustained GEMM load before the headline's warm-up and timed launches.
+    table = None if args.no_configs else config_table(set(heads), args.config_steps, args.config_warmup)
+
     results = {}
     for dtype in (["int8", "bf16"] if args.only is None else [args.only]):
         w = Workload(dtype, S, S, S)
         ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
         r = summarize(w, ms, kavg, kmin)
         r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
-        if dtype == (args.only or "int8") and not args.no_cpu_baseline:
+        if not args.no_cpu_baseline:
             r["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+            r["parity_full"] = parity_full(w)
+            w.oracle_rows = None
         results[dtype] = (w, r)
         print(f"[bench] {dtype} {S}^3: {r['value']} {r['unit']} ({r['pct_dense_peak']}% of dense peak), "
               f"kernel {r['kernel_ms_avg']} ms, plan {r['plan']}", file=sys.stderr, flush=True)
@@ -538,13 +662,18 @@ def main():
         "pct_dense_peak": hr["pct_dense_peak"],
         "kernel_ms_avg": hr["kernel_ms_avg"],
         "parity_sample_ok": hr["parity_sample_ok"],
+        "parity_full_ok": (hr.get("parity_full") or {}).get("ok"),
+        "parity_full": hr.get("parity_full"),
         "roofline": hr["roofline"],
         "cpu_baseline": hr.get("cpu_baseline"),
     }
     for dtype, (w, r) in results.items():
         if dtype != head_dtype:
-            line[dtype] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg", "pct_dense_peak",
-                                            "plan", "split_k", "parity_sample_ok", "roofline")}
+            line[dtype] = {k: r.get(k) for k in ("value", "unit", "ms_per_step", "kernel_ms_avg", "pct_dense_peak",
+                                                "plan", "split_k", "parity_sample_ok", "parity_full", "roofline",
+                                                "cpu_baseline")}
+    if table is not None:
+        line["configs"] = table
     if ceiling:
         line["mfma_ceiling"] = {"method": "gemm_probe_mfma: only the GEMM's MFMA instructions on random "
                                           "operands held in registers, one 8-wave workgroup per CU, no memory "

@@ -187,3 +187,36 @@ def test_full_size_8192_reduced_outputs(dtype):
     else:
         C = run_epilogue("bf16", A, B, pad=0)
         check_bf16(np.ascontiguousarray(A[rows]), B, np.ascontiguousarray(C[rows]))
+
+
+@pytest.mark.parametrize("cfg", [0, 10, 16, 20])
+def test_bf16_infinities_and_nans_propagate(cfg):
+    """Infinite and NaN operands: every output is NaN, +inf, -inf or finite exactly where the
+    oracle's exact sum is (IEEE sums of the same products; the class of such a sum does not
+    depend on the summation order while the finite part cannot overflow, as here), through the
+    fp32 output and the bf16 output, whose rounding must keep a NaN a NaN."""
+    rng = np.random.default_rng(40 + cfg)
+    M, K, N = 64, 96, 80
+    a = rng.integers(-4, 5, size=(M, K)).astype(np.float32)
+    bvals = np.array([-4, -3, -2, -1, 1, 2, 3, 4], dtype=np.float32)
+    bmat = bvals[rng.integers(0, 8, size=(K, N))]
+    a[3, 5] = np.inf
+    a[7, 1] = -np.inf
+    a[11, 9] = np.nan
+    a[13, 2], a[13, 40] = np.inf, -np.inf      # +inf and -inf products meet: NaN or inf by sign
+    a[20, 0] = np.inf
+    bmat[0, 17] = 0.0                          # inf * 0 = NaN in one column of row 20
+    A, B = inputs.bf16_bits_from_f32(a), inputs.bf16_bits_from_f32(bmat)
+    ref = oracle.get().gemm_bf16_f64(A, B)
+    g.force(BF, b.GEMM_KERNEL_AUTO, cfg)
+    C = g.gemm_gpu(BF, A, B).astype(np.float64)
+    assert np.array_equal(np.isnan(C), np.isnan(ref)), "NaN positions differ"
+    fin = np.isfinite(ref)
+    assert np.array_equal(C[~np.isnan(ref) & ~fin], ref[~np.isnan(ref) & ~fin]), "infinities differ"
+    assert np.array_equal(C[fin], ref[fin]), "finite (integer-valued) outputs differ"
+    assert np.isnan(ref).any() and (np.isinf(ref) & (ref > 0)).any() and (np.isinf(ref) & (ref < 0)).any()
+    Cb = run_epilogue("bf16", A, B)
+    nan_b = ((Cb & 0x7F80) == 0x7F80) & ((Cb & 0x007F) != 0)
+    assert np.array_equal(nan_b, np.isnan(ref)), "bf16 NaN positions differ"
+    ref_bits = oracle.get().round_bf16(ref)
+    assert np.array_equal(Cb[~np.isnan(ref)], ref_bits[~np.isnan(ref)]), "bf16 non-NaN outputs differ"

@@ -76,7 +76,7 @@ def test_every_config_matches_oracle(dtype, config, split, reduce):
             assert g.call(dtype, M, N, K, dA, lda, dB, ldb, dC, ldc) == b.GEMM_ERR_UNSUPPORTED
 
 
-@pytest.mark.parametrize("config", [0, 2, 3, 5, 6, 8, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 28, 29, 30, 31, 32, 33, 34, 35, 36, 37, 38, 39, 40])
+@pytest.mark.parametrize("config", [c for c in range(41) if c not in (26, 27)])
 def test_bf16_integer_valued_is_exact(config):
     """Integer-valued bf16 in [-8, 8]: the fp32 result is exact whatever the order."""
     M, N, K = 200, 264, 4096
