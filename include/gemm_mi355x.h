@@ -46,6 +46,8 @@
  *                           given shape / alignment.
  *   GEMM_ERR_NO_MEMORY      the split-K workspace could not be allocated.
  *   GEMM_ERR_HIP            a HIP launch/runtime error.
+ *   GEMM_ERR_SCRATCH_LIMIT  (gemm_bf16_f32_noalloc only) the plan's split-K
+ *                           partials exceed its fixed scratch.
  * M == 0 or N == 0 is a successful no-op.  K == 0 writes zeros (empty sum).
  * Pointers or strides that are not 16-byte aligned are accepted and routed to
  * an alignment-agnostic kernel (slower, same result).
@@ -64,7 +66,8 @@ typedef enum {
     GEMM_ERR_INVALID_VALUE = -1,
     GEMM_ERR_UNSUPPORTED = -2,
     GEMM_ERR_HIP = -3,
-    GEMM_ERR_NO_MEMORY = -4
+    GEMM_ERR_NO_MEMORY = -4,
+    GEMM_ERR_SCRATCH_LIMIT = -5  /* gemm_bf16_f32_noalloc: plan needs more than its scratch */
 } gemm_status_t;
 
 typedef enum {
@@ -129,6 +132,25 @@ int gemm_bf16_f32(int64_t M, int64_t N, int64_t K,
                   const uint16_t *A, int64_t lda,
                   const uint16_t *B, int64_t ldb,
                   float *C, int64_t ldc, void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): gemm_bf16_f32 with the
+ * same arguments, plan and result (bit for bit: the same kernels sum in the same
+ * order), except that a split-K plan keeps its partial sums and per-tile arrival
+ * counters in a fixed 16 MiB array of device memory that the library holds for
+ * each GPU it runs on until the process ends (64 KiB of counters, the rest for
+ * partials: split_k * M * N * 4 bytes must fit in 16 MiB - 64 KiB).  It never
+ * calls hipMalloc, hipFree or an allocating library routine; the counters are
+ * cleared by a fill kernel on `stream` at each split-K call.  A plan whose
+ * partials do not fit returns GEMM_ERR_SCRATCH_LIMIT before anything is queued.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time on
+ * one GPU (different streams, or host threads) race on it and must not be
+ * issued; calls queued in order on one stream are safe.  Other errors as
+ * gemm_bf16_f32. */
+int gemm_bf16_f32_noalloc(int64_t M, int64_t N, int64_t K,
+                          const uint16_t *A, int64_t lda,
+                          const uint16_t *B, int64_t ldb,
+                          float *C, int64_t ldc, void *stream);
 
 /* C = A . Bt^T with B stored column-major: C[i*ldc + j] = sum_k A[i*lda + k] *
  * Bt[j*ldbt + k].  Same results, ownership, errors and execution as

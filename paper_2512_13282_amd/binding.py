@@ -5,7 +5,8 @@ their column-major-B forms ``gemm_i8_i32_bt`` and ``gemm_bf16_f32_bt``, the
 reduced-precision-output forms ``gemm_i8_i8``, ``gemm_i8_i16``, ``gemm_bf16_bf16``
 and their ``*_bt`` forms, ``gemm_plan``,
 ``gemm_plan_bt``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
-``gemm_status_string``, ``gemm_version``, and the measurement aid ``gemm_probe_mfma``)
+``gemm_status_string``, ``gemm_version``, the no-allocation ``gemm_bf16_f32_noalloc``
+and the measurement aid ``gemm_probe_mfma``)
 take plain integers and device addresses exactly as the C ABI does.  The two
 torch helpers (``mm_i8_i32``, ``mm_bf16_f32``) only read ``data_ptr()``,
 strides and the current HIP stream of torch tensors and call the same entry
@@ -25,6 +26,7 @@ GEMM_ERR_INVALID_VALUE = -1
 GEMM_ERR_UNSUPPORTED = -2
 GEMM_ERR_HIP = -3
 GEMM_ERR_NO_MEMORY = -4
+GEMM_ERR_SCRATCH_LIMIT = -5
 
 GEMM_DTYPE_I8_I32 = 0
 GEMM_DTYPE_BF16_F32 = 1
@@ -41,7 +43,7 @@ EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt"
             "gemm_i8_i8", "gemm_i8_i16", "gemm_bf16_bf16", "gemm_i8_i8_bt", "gemm_i8_i16_bt",
             "gemm_bf16_bf16_bt", "gemm_plan",
             "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",
-            "gemm_status_string", "gemm_version", "gemm_probe_mfma")
+            "gemm_status_string", "gemm_version", "gemm_probe_mfma", "gemm_bf16_f32_noalloc")
 
 
 class PlanInfo(ctypes.Structure):
@@ -91,6 +93,8 @@ def lib() -> ctypes.CDLL:
         l.gemm_i8_i32_bt.restype = i32
         l.gemm_bf16_f32_bt.argtypes = gemm_args
         l.gemm_bf16_f32_bt.restype = i32
+        l.gemm_bf16_f32_noalloc.argtypes = gemm_args
+        l.gemm_bf16_f32_noalloc.restype = i32
         shift_args = [i64, i64, i64, p, i64, p, i64, p, i64, i32, p]
         for name in ("gemm_i8_i8", "gemm_i8_i16", "gemm_i8_i8_bt", "gemm_i8_i16_bt"):
             getattr(l, name).argtypes = shift_args
@@ -127,6 +131,10 @@ def gemm_i8_i32(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
 
 def gemm_bf16_f32(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
     return lib().gemm_bf16_f32(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, stream or None)
+
+
+def gemm_bf16_f32_noalloc(M, N, K, A, lda, B, ldb, C, ldc, stream=0) -> int:
+    return lib().gemm_bf16_f32_noalloc(M, N, K, A or None, lda, B or None, ldb, C or None, ldc, stream or None)
 
 
 def gemm_i8_i32_bt(M, N, K, A, lda, Bt, ldbt, C, ldc, stream=0) -> int:

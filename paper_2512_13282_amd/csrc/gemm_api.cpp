@@ -119,7 +119,7 @@ int plan_for(const Problem &p, Plan *out) {
 
 int run(int32_t dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
         const void *B, int64_t ldb, void *C, int64_t ldc, void *stream,
-        int32_t epilogue = gemm::EPI_NONE, int32_t shift = 0) {
+        int32_t epilogue = gemm::EPI_NONE, int32_t shift = 0, bool static_scratch = false) {
     Problem p{dtype, M, N, K, lda, ldb, ldc, uintptr_t(A), uintptr_t(B), uintptr_t(C), trans_b};
     const int64_t c_esize = epilogue == gemm::EPI_I8 ? 1 : (epilogue == gemm::EPI_NONE ? 4 : 2);
     if (shift < 0 || shift > 31) return GEMM_ERR_INVALID_VALUE;
@@ -151,8 +151,9 @@ int run(int32_t dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, const v
     a.shift = shift;
     if (pl.grid > 0x7fffffff || pl.tiles_m > 0x7fffffff || pl.tiles_n > 0x7fffffff)
         return GEMM_ERR_UNSUPPORTED;
-    const int lr = gemm::launch_gemm(a, pl.config, pl.grid, stream);
+    const int lr = gemm::launch_gemm(a, pl.config, pl.grid, stream, static_scratch);
     if (lr == gemm::LAUNCH_NO_MEMORY) return GEMM_ERR_NO_MEMORY;
+    if (lr == gemm::LAUNCH_SCRATCH_LIMIT) return GEMM_ERR_SCRATCH_LIMIT;
     if (lr != gemm::LAUNCH_OK) return GEMM_ERR_HIP;
     return GEMM_OK;
 }
@@ -169,6 +170,11 @@ int gemm_i8_i32(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, c
 int gemm_bf16_f32(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *B,
                   int64_t ldb, float *C, int64_t ldc, void *stream) {
     return run(gemm::DT_BF16, 0, M, N, K, A, lda, B, ldb, C, ldc, stream);
+}
+
+int gemm_bf16_f32_noalloc(int64_t M, int64_t N, int64_t K, const uint16_t *A, int64_t lda, const uint16_t *B,
+                          int64_t ldb, float *C, int64_t ldc, void *stream) {
+    return run(gemm::DT_BF16, 0, M, N, K, A, lda, B, ldb, C, ldc, stream, gemm::EPI_NONE, 0, true);
 }
 
 int gemm_i8_i32_bt(int64_t M, int64_t N, int64_t K, const int8_t *A, int64_t lda, const int8_t *Bt,
@@ -301,6 +307,9 @@ const char *gemm_status_string(int status) {
         case GEMM_ERR_UNSUPPORTED: return "GEMM_ERR_UNSUPPORTED: no kernel can run this plan";
         case GEMM_ERR_HIP: return "GEMM_ERR_HIP: HIP launch or runtime error";
         case GEMM_ERR_NO_MEMORY: return "GEMM_ERR_NO_MEMORY: split-K workspace allocation failed";
+        case GEMM_ERR_SCRATCH_LIMIT:
+            return "GEMM_ERR_SCRATCH_LIMIT: the plan's split-K partials exceed the fixed scratch of "
+                   "gemm_bf16_f32_noalloc";
         default: return "unknown gemm status";
     }
 }

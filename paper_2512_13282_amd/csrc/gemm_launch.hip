@@ -128,7 +128,38 @@ int release_workspaces() {
     return rc;
 }
 
-int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr) {
+// Split-K scratch of the entry point that allocates nothing (gemm_bf16_f32_noalloc):
+// a fixed array in device memory, one copy per GPU the library runs on, held until
+// the process ends.  Host code never uses the array's name as an address (on the
+// host it only stands for the symbol): the device address of each GPU's copy comes
+// from hipGetSymbolAddress, taken once per device with that device current, and is
+// the only form of it that kernels and fills receive.  Every call on a GPU shares
+// that GPU's copy, so calls that overlap in time on one GPU race on it.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, uint8_t *> g_scratch_ptr;   // device -> device address of its copy of `scratch`
+}  // namespace
+
+static int static_scratch_address(uint8_t **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return LAUNCH_HIP_ERROR;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch_ptr.find(dev);
+    if (it == g_scratch_ptr.end()) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return LAUNCH_HIP_ERROR;
+        }
+        it = g_scratch_ptr.emplace(dev, static_cast<uint8_t *>(p)).first;
+    }
+    *out = it->second;
+    return LAUNCH_OK;
+}
+
+int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr, bool static_scratch) {
     hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
     KernelArgs args = a;
     args.workspace = nullptr;
@@ -136,8 +167,26 @@ int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr
     if (args.split_k > 1) {
         const size_t bytes = size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
         const int64_t tiles = args.reduce_in_kernel ? int64_t(args.tiles_m) * args.tiles_n : 0;
-        const int rc = acquire_workspace(stream, bytes, tiles, &args.workspace, &args.counters);
-        if (rc != LAUNCH_OK) return rc;
+        if (static_scratch) {
+            if (bytes > size_t(kStaticScratchBytes - kScratchCounterBytes) || tiles * 4 > kScratchCounterBytes)
+                return LAUNCH_SCRATCH_LIMIT;
+            uint8_t *base = nullptr;
+            const int rc = static_scratch_address(&base);
+            if (rc != LAUNCH_OK) return rc;
+            args.counters = reinterpret_cast<uint32_t *>(base);
+            args.workspace = base + kScratchCounterBytes;
+            // The array keeps the previous call's contents: the arrival counters must start
+            // at zero (a fill kernel, which a stream capture records like any launch).
+            if (tiles > 0) {
+                int64_t blocks = (tiles + 255) / 256;
+                hipLaunchKernelGGL(zero_u32_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, args.counters,
+                                   tiles);
+                if (hipGetLastError() != hipSuccess) return LAUNCH_HIP_ERROR;
+            }
+        } else {
+            const int rc = acquire_workspace(stream, bytes, tiles, &args.workspace, &args.counters);
+            if (rc != LAUNCH_OK) return rc;
+        }
     }
     hipError_t e = args.dtype == DT_I8 ? launch_config<DT_I8>(cfg, args, grid, stream)
                                        : launch_config<DT_BF16>(cfg, args, grid, stream);

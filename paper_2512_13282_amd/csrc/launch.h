@@ -31,10 +31,18 @@ struct KernelArgs {
 // to the nearest bf16, ties to even.
 enum { EPI_NONE = 0, EPI_I8 = 1, EPI_I16 = 2, EPI_BF16 = 3 };
 
-enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2 };
+enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2, LAUNCH_SCRATCH_LIMIT = 3 };
 
-// Queues the plan's kernels on `stream` (a hipStream_t).  Never synchronizes.
-int launch_gemm(const KernelArgs &a, int32_t config, int64_t grid, void *stream);
+// The fixed split-K scratch of the entry point that allocates nothing: per device,
+// kScratchCounterBytes of per-tile arrival counters followed by the partial planes.
+constexpr int64_t kStaticScratchBytes = int64_t(16) << 20;
+constexpr int64_t kScratchCounterBytes = int64_t(64) << 10;
+
+// Queues the plan's kernels on `stream` (a hipStream_t).  Never synchronizes.  With
+// static_scratch a split-K plan takes its partials and counters from the library's
+// fixed per-device scratch instead of the per-stream workspace (no allocation), or
+// returns LAUNCH_SCRATCH_LIMIT, before queueing anything, when they do not fit.
+int launch_gemm(const KernelArgs &a, int32_t config, int64_t grid, void *stream, bool static_scratch = false);
 
 // Frees every cached split-K workspace (all devices and streams) after
 // synchronising each device that holds one.

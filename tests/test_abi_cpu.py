@@ -32,13 +32,13 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     for rc in (b.GEMM_OK, b.GEMM_ERR_INVALID_VALUE, b.GEMM_ERR_UNSUPPORTED, b.GEMM_ERR_HIP,
-               b.GEMM_ERR_NO_MEMORY):
+               b.GEMM_ERR_NO_MEMORY, b.GEMM_ERR_SCRATCH_LIMIT):
         assert b.gemm_status_string(rc).startswith("GEMM_")
     assert "unknown" in b.gemm_status_string(12345)
     assert "gfx950" in b.gemm_version()
 
 
-@pytest.mark.parametrize("fn", [b.gemm_i8_i32, b.gemm_bf16_f32])
+@pytest.mark.parametrize("fn", [b.gemm_i8_i32, b.gemm_bf16_f32, b.gemm_bf16_f32_noalloc])
 @pytest.mark.parametrize("args", [
     (-1, 4, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4),     # negative M
     (4, -1, 4, FAKE_A, 4, FAKE_B, 4, FAKE_C, 4),     # negative N
@@ -62,7 +62,7 @@ def test_bf16_pointer_alignment():
     assert b.gemm_bf16_f32(4, 4, 4, FAKE_A + 1, 4, FAKE_B, 4, FAKE_C, 4, 0) == b.GEMM_ERR_INVALID_VALUE
 
 
-@pytest.mark.parametrize("fn", [b.gemm_i8_i32, b.gemm_bf16_f32])
+@pytest.mark.parametrize("fn", [b.gemm_i8_i32, b.gemm_bf16_f32, b.gemm_bf16_f32_noalloc])
 def test_empty_output_is_a_noop(fn):
     # M == 0 or N == 0: nothing to write, success without touching the GPU; pointers of
     # empty operands may be null, those of non-empty ones may not
