@@ -472,7 +472,30 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, uint8_t 
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LDS_AS void *)lds_wave_base, 16, int(voff), 0, 0, 0);
 }
 
-__device__ __forceinline__ int ring_swz(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+// Swizzle of the ring's 64-byte rows (A, and column-major B): chunk c of row r sits at
+// chunk c ^ ((r >> 2) & 3).  Measured on gfx950 with a read-throughput probe (16 waves
+// issuing the fragment reads of a 32-row block): 4 cycles per 16-byte-per-lane read,
+// the conflict-free rate, where ((r >> 1) ^ (r >> 3)) & 3 took 8 and no swizzle 16.
+// Period 16 in r, so the tiles 32 rows apart read at fixed offsets.
+__device__ __forceinline__ int ring_swz(int row) { return (row >> 2) & 3; }
+
+// Swizzle of row-major B rows (k) for the transpose reads, by row width: chunk c of
+// row k sits at chunk c ^ ring_bswz(k).  Rows of 16 or more chunks use bswz; the
+// narrow rows of the small-N ring tiles use functions found by measuring every
+// GF(2)-linear map of k's low row bits onto the chunk bits with the same probe
+// (each at 2.5 cycles per 8-byte-per-lane read; unswizzled rows took 4.2-8.2):
+//   int8, 8 chunks (N tile 128):  k & 7
+//   int8, 4 chunks (N tile 64):   (k & 4) >> 1
+//   bf16, 8 chunks (N tile 64):   k1 | k0 << 1 | k1 << 2   (k0, k1: the low bits of k)
+// Each depends only on the row within one transpose read's 4- or 8-row block.
+template <int DT, int CPR>
+__device__ __forceinline__ int ring_bswz(int k) {
+    if constexpr (CPR >= 16) return bswz<DT>(k);
+    else if constexpr (DT == DT_I8 && CPR == 8) return k & 7;
+    else if constexpr (DT == DT_I8 && CPR == 4) return (k & 4) >> 1;
+    else if constexpr (DT == DT_BF16 && CPR == 8) return ((k >> 1) & 1) | ((k & 1) << 1) | (((k >> 1) & 1) << 2);
+    else return 0;
+}
 
 // Buffer resource as four dwords (base, stride 0, size in bytes, raw-access flags)
 // for the inline-assembly load below.

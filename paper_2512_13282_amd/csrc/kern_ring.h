@@ -29,10 +29,10 @@ namespace gemm {
 // LDS reads and global loads are issued in a fixed interleaved order.
 //
 // LDS, per slot: A as BM rows of 64 K-bytes, the 16-byte chunk c of row r at
-// chunk c ^ ga(r), ga(r) = ((r >> 1) ^ (r >> 3)) & 3, which keeps the fragment
-// reads of any 8 (and any 16) consecutive rows on distinct banks; B row-major
-// as 64 / E rows (k) of BN * E bytes with gemm_lds_kernel's swizzle (rows of
-// at least 256 bytes; narrower rows unswizzled), or column-major (BT) like A.  Every slot of every iteration issues the same
+// chunk c ^ ring_swz(r); B row-major as 64 / E rows (k) of BN * E bytes, chunk c
+// of row k at c ^ ring_bswz(k) (gemm_lds_kernel's swizzle for rows of at least
+// 256 bytes, measured conflict-free functions for the narrower rows), or
+// column-major (BT) like A.  Every slot of every iteration issues the same
 // number of loads (slots past the end of the K range get an empty resource and
 // load zeros without touching memory), so the wait before each barrier is a
 // fixed count of this wave's loads still allowed in flight.
@@ -61,9 +61,7 @@ void gemm_ring_kernel(KernelArgs args) {
     constexpr int LPS = A_INSTR + B_INSTR;                // loads per wave per slot
     constexpr int B_ROWS_PER_KB = 1024 / B_PITCH;
     constexpr int B_CPR = B_PITCH / 16;                   // 16-byte chunks per B row
-    // Row-major B rows of 16 or more chunks are swizzled for conflict-free transpose
-    // reads; narrower rows (small BN) are stored as they are.
-    constexpr bool B_SWZ = !BT && B_CPR >= 16;
+    // Row-major B rows are swizzled for conflict-free transpose reads (ring_bswz, by row width).
     constexpr int NREAD = TM + (BT ? TN : 2 * TN);        // LDS reads per k-step
     static_assert(NB >= 3 && NB <= 8, "ring depth");
     static_assert(TM >= 1 && TN >= 1, "wave tile of at least one 32 x 32 MFMA tile");
@@ -129,7 +127,7 @@ void gemm_ring_kernel(KernelArgs args) {
             b_voff[i] = uint32_t(row * ldb_b + c * 16);
         } else {
             const int row = (i * WAVES + wave) * B_ROWS_PER_KB + lane / B_CPR;
-            const int c = (lane % B_CPR) ^ (B_SWZ ? bswz<DT>(row) : 0);
+            const int c = (lane % B_CPR) ^ ring_bswz<DT, B_CPR>(row);
             b_chunk[i] = 0;
             b_voff[i] = (n0 + int64_t(c) * VECE < N) ? uint32_t(row * ldb_b + c * 16) : kOOB;
         }
@@ -190,7 +188,7 @@ void gemm_ring_kernel(KernelArgs args) {
     const int tr_row = DT == DT_BF16 ? (g16 >> 2) : (g16 >> 1);
     const int tr_colb = (DT == DT_BF16 ? (g16 & 3) * 8 : (g16 & 1) * 8) + (grp & 1) * 16 * E;
     const int tr_khalf = (grp >> 1) * (KSTEP / 2);
-    const int bz = B_SWZ ? bswz<DT>(tr_row) : 0;
+    const int bz = BT ? 0 : ring_bswz<DT, B_CPR>(tr_row);
     int b_fo[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {

@@ -20,7 +20,10 @@ row-major, plus the skinny and 8192^3 workloads with B stored column-major
 (the *_bt entry points).  A shapes file lists [dtype, M, K, N] or
 [dtype, M, K, N, "bt"].  Memory-bound shapes (M < 256) are timed cold: the
 launches rotate through enough copies of B to exceed the 256 MB last-level
-cache.
+cache.  The two cache-sized workloads (int8 256^3, bf16 1024^3) are timed as
+lone launches after a 512 MiB flush.  Back-to-back launches queue behind a
+spin kernel so that short kernels are timed on the GPU, not on the host's
+launch rate.
 """
 from __future__ import annotations
 
@@ -37,11 +40,31 @@ SPLITS_SMALL_M = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 SPLITS_LARGE = (1, 2, 3, 4)
 
 
+_SPIN_RATE = None
+
+
+def _spin_ahead(launches, host_us_per_launch=80.0):
+    """Queues a spin kernel long enough for the host to enqueue `launches` more launches behind
+    it, so that short kernels run back to back and are timed on the GPU, not on the host's
+    launch rate; the spin's cycles per microsecond are measured once."""
+    global _SPIN_RATE
+    import torch
+    if _SPIN_RATE is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.cuda._sleep(1_000_000)
+        e1.record()
+        torch.cuda.synchronize()
+        _SPIN_RATE = 1_000_000 / max(e0.elapsed_time(e1) * 1e3, 1.0)
+    torch.cuda._sleep(int(_SPIN_RATE * host_us_per_launch * launches))
+
+
 def _time(fn, copies, iters):
     import torch
     for i in range(3):
         fn(i % copies)
     torch.cuda.synchronize()
+    _spin_ahead(iters)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
     for i in range(iters):
         ev[i][0].record()
@@ -51,12 +74,32 @@ def _time(fn, copies, iters):
     return float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e3   # us
 
 
+def _time_flushed(fn, iters):
+    """Median time of single launches, each after a 512 MiB write that evicts the operands
+    from the L2s and the last-level cache: the protocol for shapes whose operands fit in the
+    caches (a lone GEMM of that size finds them cold)."""
+    import torch
+    scratch = torch.empty(128 * 1024 * 1024, dtype=torch.float32, device="cuda:0")
+    fn(0)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    for i in range(iters):
+        scratch.fill_(float(i))
+        ev[i][0].record()
+        fn(0)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    del scratch
+    return float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e3   # us
+
+
 def _time_sustained(fn, copies, warmup, iters):
     """Average time of `iters` back-to-back launches after `warmup` untimed ones: the regime
     of a long run of GEMMs, in which the chip's power manager has settled."""
     import torch
     for i in range(warmup):
         fn(i % copies)
+    _spin_ahead(iters, 40.0)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(iters):
@@ -67,7 +110,7 @@ def _time_sustained(fn, copies, warmup, iters):
 
 
 def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bool = False,
-               confirm: int = 3, rounds: int = 3):
+               confirm: int = 3, rounds: int = 3, cold_single: bool = False):
     import torch
     from . import binding as b
     d = b.GEMM_DTYPE_I8_I32 if dtype == "int8" else b.GEMM_DTYPE_BF16_F32
@@ -112,7 +155,7 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
                         continue
                     if plan["split_k"] != split and split != 1:
                         continue            # clamped duplicate
-                    us = _time(run, copies, iters)
+                    us = _time_flushed(run, iters) if cold_single else _time(run, copies, iters)
                     results.append({"config": cfg, "split": plan["split_k"],
                                     "reduce": plan["reduce_in_kernel"] if plan["split_k"] > 1 else -1,
                                     "name": plan["name"], "us": us})
@@ -127,7 +170,7 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
                 for t, cand in enumerate(top):
                     b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, cand["config"], cand["split"])
                     b.gemm_force_reduce(d, cand["reduce"] if cand["split"] > 1 else -1)
-                    times[t].append(_time_sustained(run, copies, 30, 50))
+                    times[t].append(_time_flushed(run, 30) if cold_single else _time_sustained(run, copies, 30, 50))
             for t, cand in enumerate(top):
                 cand["us_sustained"] = float(np.median(times[t]))
     finally:
@@ -174,7 +217,9 @@ def main():
     for shape in shapes:
         dtype, M, K, N = shape[:4]
         bt = len(shape) > 4 and shape[4] == "bt"
-        best, res = tune_shape(dtype, M, N, K, args.iters, bt=bt, confirm=args.confirm)
+        # Shapes whose operands fit in the caches are timed as lone launches on cold caches.
+        cold_single = (dtype, M, K, N) in inputs.SMALL
+        best, res = tune_shape(dtype, M, N, K, args.iters, bt=bt, confirm=args.confirm, cold_single=cold_single)
         entries.append({"dtype": 0 if dtype == "int8" else 1, "M": M, "N": N, "K": K, "trans_b": int(bt), **best})
         everything.append({"dtype": dtype, "M": M, "K": K, "N": N, "bt": bt, "results": res})
     write_inc(entries, args.out)
