@@ -190,17 +190,33 @@ def spin_ahead(launches: int, host_us_per_launch: float = 80.0) -> None:
     torch.cuda._sleep(int(_SPIN_RATE * host_us_per_launch * launches))
 
 
-def time_workload(w: Workload, steps: int, warmup: int, prefill: bool = False):
-    """W untimed launches, then `steps` launches with HIP events on the launch stream around
-    each.  Returns (wall ms per step, mean kernel ms, min kernel ms).  With `prefill` a spin
-    kernel queued first keeps the GPU from waiting on the host between short launches (the
-    wall time then includes the spin and is not meaningful)."""
+def time_back_to_back(w: Workload, steps: int, warmup: int):
+    """W untimed launches; then, behind a spin kernel that lets the host queue them all,
+    `steps` back-to-back launches between two HIP events on the launch stream.  Returns the
+    GPU time per launch in ms (kernel plus the GPU's own gap between kernels; events around
+    every launch would add their own overhead, a few microseconds per launch)."""
     import torch
     for _ in range(warmup):
         w.launch()
     torch.cuda.synchronize()
-    if prefill:
-        spin_ahead(steps)
+    spin_ahead(steps, 40.0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(w.stream)
+    for _ in range(steps):
+        w.launch()
+    e1.record(w.stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    return ms, ms, ms
+
+
+def time_workload(w: Workload, steps: int, warmup: int):
+    """W untimed launches, then `steps` launches with HIP events on the launch stream around
+    each.  Returns (wall ms per step, mean kernel ms, min kernel ms)."""
+    import torch
+    for _ in range(warmup):
+        w.launch()
+    torch.cuda.synchronize()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     t0 = time.perf_counter()
@@ -320,9 +336,10 @@ def config_table(skip, steps: int, warmup: int):
     HIP events on the launch stream.  Shapes whose operands fit in the caches (int8 256^3,
     bf16 1024^3) are timed cold, one launch at a time after a 512 MiB flush; the skinny
     (memory-bound) shapes rotate through enough copies of B that more than 512 MB is read
-    between reuses of a copy; the rest are timed warm, back to back.  Back-to-back launches are
-    queued behind a spin kernel so that each is timed on the GPU rather than waiting on the
-    host's next launch (a Python launch takes longer than the smallest kernels).  Each row carries its
+    between reuses of a copy; the rest are timed warm.  Back-to-back launches are queued behind
+    a spin kernel and timed between two events, so that each is timed on the GPU rather than
+    waiting on the host's next launch (a Python launch takes longer than the smallest kernels).
+    Each row carries its
     protocol, plan, roofline fraction and a parity check of sampled output rows."""
     import torch
     from paper_2512_13282_amd import inputs
@@ -338,7 +355,7 @@ def config_table(skip, steps: int, warmup: int):
             ms, kavg, kmin = time_workload_flushed(w, steps, warmup)
             proto = "cold: 512 MiB flush before each launch, launches timed one by one"
         else:
-            ms, kavg, kmin = time_workload(w, steps, warmup, prefill=True)
+            ms, kavg, kmin = time_back_to_back(w, steps, warmup)
             proto = (f"cold: back to back, B rotated over {copies} copies (> 512 MB between reuses)"
                      if skinny else "warm: back to back, operands resident")
         r = summarize(w, ms, kavg, kmin)
@@ -425,7 +442,8 @@ def mfma_ceiling(dtype: str, iters: int = 20000, launches: int = 3) -> dict:
 
 
 def write_traffic(fetch_csv: str, write_csv: str) -> None:
-    """HBM bytes per launch of the timed GEMM kernels from rocprofv3 counter CSVs.
+    """L2 -> fabric bytes (last-level cache and HBM) per launch of the timed GEMM kernels, from
+    rocprofv3 counter CSVs.
 
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by the factor that
     makes them read the known traffic of the plain 512 MiB copy profiled in the same
@@ -477,6 +495,9 @@ def write_traffic(fetch_csv: str, write_csv: str) -> None:
     out = {"kernel_source_sha256": kernel_sha(), "fetch_scale": round(f_scale, 4),
            "write_scale": round(w_scale, 4), "copy_probe_bytes": COPY_PROBE_BYTES,
            "counters": "rocprofv3 --pmc FETCH_SIZE / --pmc WRITE_SIZE, KiB per dispatch, averaged",
+           "what": "bytes the XCD L2 caches request from / write to the fabric behind them, i.e. the "
+                   "256 MB last-level cache (MALL) and HBM together: an upper bound on HBM traffic "
+                   "(the counters do not separate MALL hits from HBM accesses)",
            "workloads": workloads}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:

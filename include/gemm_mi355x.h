@@ -44,7 +44,11 @@
  *                           non-empty; C overlapping A or B in memory.
  *   GEMM_ERR_UNSUPPORTED    a forced plan (gemm_force_plan) that cannot run the
  *                           given shape / alignment.
- *   GEMM_ERR_NO_MEMORY      the split-K workspace could not be allocated.
+ *   GEMM_ERR_NO_MEMORY      the split-K workspace could not be allocated (nothing
+ *                           is queued; a later call allocates afresh).  Setting
+ *                           GEMM_MI355X_TEST_FAIL_WORKSPACE=1 in the environment
+ *                           makes every workspace allocation fail this way (a
+ *                           test hook; read at each allocation).
  *   GEMM_ERR_HIP            a HIP launch/runtime error.
  *   GEMM_ERR_SCRATCH_LIMIT  (gemm_bf16_f32_noalloc only) the plan's split-K
  *                           partials exceed its fixed scratch.

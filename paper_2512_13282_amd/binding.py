@@ -19,7 +19,9 @@ import ctypes
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libgemm_mi355x.so")
+# GEMM_MI355X_LIBRARY names another build of the same library (the sanitizer test loads a
+# host-only build of the C ABI through it); there is no fallback if the file is missing.
+LIB_PATH = os.environ.get("GEMM_MI355X_LIBRARY") or os.path.join(PKG, "libgemm_mi355x.so")
 
 GEMM_OK = 0
 GEMM_ERR_INVALID_VALUE = -1

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <stdlib.h>
+
 #include <map>
 #include <mutex>
 #include <utility>
@@ -63,12 +65,23 @@ size_t grow(size_t need, size_t have, size_t quantum) {
 }
 }  // namespace
 
+// Test hook: with GEMM_MI355X_TEST_FAIL_WORKSPACE=1 in the environment, every workspace
+// allocation the library would make fails as if the device were out of memory (the
+// caller then gets GEMM_ERR_NO_MEMORY and nothing is queued).  Read at each allocation,
+// so a process can switch it on and off.
+static bool fail_workspace_for_test() {
+    const char *e = getenv("GEMM_MI355X_TEST_FAIL_WORKSPACE");
+    return e != nullptr && e[0] == '1';
+}
+
 static int acquire_workspace(hipStream_t stream, size_t partial_bytes, int64_t tiles, void **partials,
                              uint32_t **counters) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return LAUNCH_HIP_ERROR;
     std::lock_guard<std::mutex> lk(g_ws_mu);
     Workspace &w = g_ws[{dev, reinterpret_cast<uintptr_t>(stream)}];
+    if ((w.partial_bytes < partial_bytes || w.counter_cap < tiles) && fail_workspace_for_test())
+        return LAUNCH_NO_MEMORY;
     if (w.partial_bytes < partial_bytes) {
         if (w.partials != nullptr && hipFreeAsync(w.partials, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
         w.partials = nullptr;
