@@ -509,12 +509,13 @@ def write_traffic(fetch_csv: str, write_csv: str) -> None:
 PAPER_SWEEP_SIZES = (256, 512, 1024, 2048, 3072, 4096, 6144, 8192)
 
 
-def paper_sweep_run(out_dir: str, iters: int = 5) -> dict:
+def paper_sweep_run(out_dir: str, iters: int = 10) -> dict:
     """GEMM TOPS over every (M, K, N) in PAPER_SWEEP_SIZES^3 (multiples of the 256 tile up to
     8192), both dtypes and both B layouts, with the selector's plans.  Operands are drawn on the
-    device (torch, seed 0) in the sweep's distributions and reused as views; each point is the
-    median of `iters` HIP-event-timed launches after two warm-ups.  Returns a summary; every
-    point goes to out_dir/paper_sweep.jsonl."""
+    device (torch, seed 0) in the sweep's distributions and reused as views; each point is
+    `iters` back-to-back launches after two warm-ups, queued behind a spin kernel and timed
+    between two HIP events (the GPU's time per launch).  Returns a summary; every point goes to
+    out_dir/paper_sweep.jsonl."""
     import torch
     from paper_2512_13282_amd import binding
     dev = torch.device("cuda:0")
@@ -545,14 +546,15 @@ def paper_sweep_run(out_dir: str, iters: int = 5) -> dict:
                             for _ in range(2):
                                 if call() != 0:
                                     raise RuntimeError(f"GEMM failed at {(dtype, M, K, N, bt)}")
-                            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                                  for _ in range(iters)]
-                            for a, b in ev:
-                                a.record(st)
-                                call()
-                                b.record(st)
                             torch.cuda.synchronize()
-                            ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+                            spin_ahead(iters, 40.0)
+                            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                            e0.record(st)
+                            for _ in range(iters):
+                                call()
+                            e1.record(st)
+                            torch.cuda.synchronize()
+                            ms = e0.elapsed_time(e1) / iters
                             t = 2.0 * M * N * K / (ms * 1e-3) / 1e12
                             tops.append((t, M, K, N))
                             f.write(json.dumps({"dtype": dtype, "b_layout": "col" if bt else "row", "M": M,
@@ -563,6 +565,9 @@ def paper_sweep_run(out_dir: str, iters: int = 5) -> dict:
                 key = f"{dtype}_{'col' if bt else 'row'}_major_b"
                 summary[key] = {"max": round(best[0], 1), "max_at_MKN": list(best[1:]),
                                 "median": round(float(np.median(vals)), 1),
+                                "quartiles": [round(float(np.percentile(vals, q)), 1) for q in (25, 75)],
+                                "at_or_above_4096_cube_volume_median": round(float(np.median(
+                                    [t for t, m_, k_, n_ in tops if m_ * k_ * n_ >= 4096 ** 3])), 1),
                                 "points_at_or_above_40pct_peak": int(np.sum(vals >= 0.4 * PEAK[dtype])),
                                 "unit": "TOPS" if dtype == "int8" else "TFLOP/s"}
                 print(f"[paper-sweep] {key}: max {best[0]:.1f} at M,K,N={best[1:]}, median "

@@ -106,8 +106,10 @@ def test_gemv_padded_strides_and_canaries():
 
 @pytest.mark.parametrize("dtype,M,K,N", [c for c in inputs.SKINNY if c[1] == 1],
                          ids=[f"{c[0]}-{c[2]}x{c[3]}" for c in inputs.SKINNY if c[1] == 1])
-def test_gemv_selected_for_full_size_m1(dtype, M, K, N):
-    """The full-size M = 1 workloads through the selector's plan, against the whole oracle row."""
+def test_full_size_m1_selector_plan(dtype, M, K, N):
+    """The full-size M = 1 workloads (B row-major) through the selector's plan, whichever kernel
+    it picks (a tuned ring plan at present; the row-major GEMV kernel is tested above), against
+    the whole oracle row."""
     d = I8 if dtype == "int8" else BF
     fake = 1 << 40
     plan = b.gemm_plan(d, M, N, K, K, N, N, fake, 2 * fake, 3 * fake)
