@@ -331,6 +331,32 @@ def parity_full(w: Workload):
             "rule": "max|C - C_ref| / (K max|A| max|B|) <= 1e-5"}
 
 
+def bare_read_us(w: Workload, steps: int = 50, warmup: int = 10) -> float:
+    """Microseconds a plain read of B takes (gemm_probe_read), back to back over the same
+    rotating copies of B the GEMM was timed with: what the memory-bound GEMMs are held to."""
+    import torch
+    from paper_2512_13282_amd import binding
+    nbytes = w.dBs[0].numel() * w.dBs[0].element_size()
+    threads = torch.cuda.get_device_properties(0).multi_processor_count * 2048
+    sink = torch.empty(threads, dtype=torch.int32, device="cuda:0")
+    def call(i):
+        rc = binding.gemm_probe_read(w.dBs[i % len(w.dBs)].data_ptr(), nbytes, sink.data_ptr(), threads,
+                                     w.stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(binding.gemm_status_string(rc))
+    for i in range(warmup):
+        call(i)
+    torch.cuda.synchronize()
+    spin_ahead(steps, 40.0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(w.stream)
+    for i in range(steps):
+        call(i)
+    e1.record(w.stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps
+
+
 def config_table(skip, steps: int, warmup: int):
     """Every workload of the sweep (inputs.ALL_CONFIGS) except those in `skip`, timed with
     HIP events on the launch stream.  Shapes whose operands fit in the caches (int8 256^3,
@@ -360,16 +386,23 @@ def config_table(skip, steps: int, warmup: int):
                      if skinny else "warm: back to back, operands resident")
         r = summarize(w, ms, kavg, kmin)
         ops = 2.0 * M * N * K
+        bare = bare_read_us(w) if skinny else None
         row = {"dtype": dtype, "M": M, "K": K, "N": N, "protocol": proto, "plan": r["plan"],
                "split_k": r["split_k"], "kernel_us": round(kavg * 1e3, 2),
                "value": round(ops / (kavg * 1e-3) / 1e12, 2), "unit": r["unit"],
                "pct_dense_peak": round(100.0 * ops / (kavg * 1e-3) / 1e12 / PEAK[dtype], 2),
                "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac")},
                "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))}
+        if bare is not None:
+            # a plain read of B under the same protocol (the GEMM also reads A and writes C)
+            row["bare_read_of_B_us"] = round(bare, 2)
+            row["frac_of_bare_read"] = round(bare / (kavg * 1e3), 3)
         rows.append(row)
         print(f"[configs] {dtype:4s} M={M:5d} K={K:6d} N={N:6d} {row['kernel_us']:9.1f} us {row['value']:9.2f} "
               f"{row['unit']:7s} {row['roofline']['bound']} frac={row['roofline']['frac']:.3f} plan={row['plan']} "
-              f"x{row['split_k']} ok={row['parity_sample_ok']}", file=sys.stderr, flush=True)
+              f"x{row['split_k']} ok={row['parity_sample_ok']}"
+              + (f" bare-read={row['bare_read_of_B_us']}us ({row['frac_of_bare_read']:.2f})" if "bare_read_of_B_us" in row else ""),
+              file=sys.stderr, flush=True)
         del w
         torch.cuda.empty_cache()
     return rows

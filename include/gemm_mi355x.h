@@ -266,6 +266,18 @@ typedef struct gemm_probe_info {
 int gemm_probe_mfma(int dtype, int random_operands, int32_t iters, int64_t *clocks,
                     unsigned *sink, gemm_probe_info *info, void *stream);
 
+/* ---- Measurement aid (not part of the GEMM) ------------------------------
+ * gemm_probe_read reads `bytes` bytes of device memory at `src` once (16 bytes per
+ * lane per load, grid-stride over the whole range, 8 workgroups of 256 threads per
+ * compute unit) and writes one value per thread to `sink` so that no load is
+ * skipped: bytes / duration is what a plain read of that range reaches, the
+ * reference for the memory-bound (skinny) GEMMs.  `src` and `bytes` must be
+ * multiples of 16; `sink` (device, uint32, `sink_elems` elements) must hold one
+ * value per thread: 2048 per compute unit.  Asynchronous on `stream`.  Returns
+ * GEMM_OK, GEMM_ERR_INVALID_VALUE (misaligned or negative size, NULL source with
+ * bytes > 0, sink NULL or too small) or GEMM_ERR_HIP. */
+int gemm_probe_read(const void *src, int64_t bytes, unsigned *sink, int64_t sink_elems, void *stream);
+
 /* Static description of the error code. */
 const char *gemm_status_string(int status);
 

@@ -6,7 +6,7 @@ reduced-precision-output forms ``gemm_i8_i8``, ``gemm_i8_i16``, ``gemm_bf16_bf16
 and their ``*_bt`` forms, ``gemm_plan``,
 ``gemm_plan_bt``, ``gemm_force_plan``, ``gemm_force_reduce``, ``gemm_release_workspace``,
 ``gemm_status_string``, ``gemm_version``, the no-allocation ``gemm_bf16_f32_noalloc``
-and the measurement aid ``gemm_probe_mfma``)
+and the measurement aids ``gemm_probe_mfma`` and ``gemm_probe_read``)
 take plain integers and device addresses exactly as the C ABI does.  The two
 torch helpers (``mm_i8_i32``, ``mm_bf16_f32``) only read ``data_ptr()``,
 strides and the current HIP stream of torch tensors and call the same entry
@@ -45,7 +45,8 @@ EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt"
             "gemm_i8_i8", "gemm_i8_i16", "gemm_bf16_bf16", "gemm_i8_i8_bt", "gemm_i8_i16_bt",
             "gemm_bf16_bf16_bt", "gemm_plan",
             "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",
-            "gemm_status_string", "gemm_version", "gemm_probe_mfma", "gemm_bf16_f32_noalloc")
+            "gemm_status_string", "gemm_version", "gemm_probe_mfma", "gemm_bf16_f32_noalloc",
+            "gemm_probe_read")
 
 
 class PlanInfo(ctypes.Structure):
@@ -122,6 +123,8 @@ def lib() -> ctypes.CDLL:
         l.gemm_version.restype = ctypes.c_char_p
         l.gemm_probe_mfma.argtypes = [i32, i32, ctypes.c_int32, p, p, ctypes.POINTER(ProbeInfo), p]
         l.gemm_probe_mfma.restype = i32
+        l.gemm_probe_read.argtypes = [p, i64, p, i64, p]
+        l.gemm_probe_read.restype = i32
         _lib = l
     return _lib
 
@@ -203,6 +206,10 @@ def gemm_status_string(status: int) -> str:
 
 def gemm_version() -> str:
     return lib().gemm_version().decode()
+
+
+def gemm_probe_read(src, nbytes, sink=0, sink_elems=0, stream=0) -> int:
+    return lib().gemm_probe_read(src or None, nbytes, sink or None, sink_elems, stream or None)
 
 
 def gemm_probe_mfma(dtype, random_operands, iters, clocks=0, sink=0, stream=0):

@@ -1,4 +1,5 @@
-// mfma_probe.hip -- sustained MFMA rate of this GPU on random operands.
+// mfma_probe.hip -- measurement aids: the sustained MFMA rate of this GPU on random
+// operands (gemm_probe_mfma), and the time of a plain read (gemm_probe_read).
 //
 // A measurement aid, not part of the GEMM: one workgroup of 8 waves per CU
 // (forced by its LDS request) issues only 32x32 MFMAs of the GEMM's own
@@ -104,7 +105,39 @@ __global__ __launch_bounds__(64 * kProbeWaves) void mfma_probe_kernel(int random
     }
 }
 
+// Streams `n16` 16-byte pieces of `src` once (grid-stride, four loads in flight per
+// lane), folding them into one value per thread so that nothing is skipped: the time
+// a plain read of those bytes takes, the reference for the memory-bound GEMMs.
+__global__ __launch_bounds__(256) void read_probe_kernel(const u32x4_t *__restrict__ src, int64_t n16,
+                                                         unsigned *sink) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+    int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    u32x4_t acc = {0u, 0u, 0u, 0u};
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+        const u32x4_t a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        acc ^= a ^ b ^ c ^ d;
+    }
+    for (; i < n16; i += stride) acc ^= src[i];
+    sink[int64_t(blockIdx.x) * blockDim.x + threadIdx.x] = acc.x ^ acc.y ^ acc.z ^ acc.w;
+}
+
+constexpr int kReadProbeBlocksPerCu = 8;
+
 }  // namespace
+
+extern "C" int gemm_probe_read(const void *src, int64_t bytes, unsigned *sink, int64_t sink_elems, void *stream) {
+    if (bytes < 0 || (bytes > 0 && src == nullptr) || (reinterpret_cast<uintptr_t>(src) & 15) != 0 || (bytes & 15) != 0)
+        return GEMM_ERR_INVALID_VALUE;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return GEMM_ERR_HIP;
+    const int64_t threads = int64_t(cus) * kReadProbeBlocksPerCu * 256;
+    if (sink == nullptr || sink_elems < threads) return GEMM_ERR_INVALID_VALUE;
+    hipLaunchKernelGGL(read_probe_kernel, dim3(unsigned(cus * kReadProbeBlocksPerCu)), dim3(256), 0,
+                       static_cast<hipStream_t>(stream), static_cast<const u32x4_t *>(src), bytes / 16, sink);
+    return hipGetLastError() == hipSuccess ? GEMM_OK : GEMM_ERR_HIP;
+}
 
 extern "C" int gemm_probe_mfma(int dtype, int random_operands, int32_t iters, int64_t *clocks,
                                unsigned *sink, gemm_probe_info *info, void *stream) {

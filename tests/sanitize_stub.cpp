@@ -16,3 +16,4 @@ int release_workspaces() { return LAUNCH_OK; }
 extern "C" int gemm_probe_mfma(int, int, int32_t, int64_t *, unsigned *, gemm_probe_info *, void *) {
     return GEMM_ERR_HIP;
 }
+extern "C" int gemm_probe_read(const void *, int64_t, unsigned *, int64_t, void *) { return GEMM_ERR_HIP; }
