@@ -201,21 +201,124 @@ __device__ __forceinline__ void write_c(const KernelArgs &a, int64_t idx, V v) {
     }
 }
 
-// A wave's output fragments straight into C with the epilogue EPI.  Lane l holds,
+// 4 x 4 transpose inside each group of four lanes: on entry lane q (= lane % 4)
+// holds x[k] = X[k][q], on exit x[k] = X[q][k].  Two butterfly stages, the first
+// exchanging 2 x 2 blocks with lane q ^ 2, the second single values with lane q ^ 1;
+// each stage sends two values through one DPP quad permutation apiece.  Every lane
+// of the wave must be active.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_quad(uint32_t v) {
+    return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ void quad_transpose(uint32_t (&x)[4], int lane) {
+    constexpr int XOR2 = 2 | (3 << 2) | (0 << 4) | (1 << 6);   // lane q reads lane q ^ 2
+    constexpr int XOR1 = 1 | (0 << 2) | (3 << 4) | (2 << 6);   // lane q reads lane q ^ 1
+    const bool hi = (lane & 2) != 0, odd = (lane & 1) != 0;
+    const uint32_t r0 = dpp_quad<XOR2>(hi ? x[0] : x[2]), r1 = dpp_quad<XOR2>(hi ? x[1] : x[3]);
+    const uint32_t z0 = hi ? r0 : x[0], z1 = hi ? r1 : x[1], z2 = hi ? x[2] : r0, z3 = hi ? x[3] : r1;
+    const uint32_t u0 = dpp_quad<XOR1>(odd ? z0 : z1), u1 = dpp_quad<XOR1>(odd ? z2 : z3);
+    x[0] = odd ? u0 : z0;
+    x[1] = odd ? z1 : u0;
+    x[2] = odd ? u1 : z2;
+    x[3] = odd ? z3 : u1;
+}
+
+// Four consecutive outputs of one row as one non-temporal store (16, 8 or 4 bytes).
+template <typename O>
+__device__ __forceinline__ void store4_nt(O *dst, const O (&c)[4]) {
+    if constexpr (sizeof(O) == 4) {
+        const u32x4_t v{__builtin_bit_cast(uint32_t, c[0]), __builtin_bit_cast(uint32_t, c[1]),
+                        __builtin_bit_cast(uint32_t, c[2]), __builtin_bit_cast(uint32_t, c[3])};
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t *>(dst));
+    } else if constexpr (sizeof(O) == 2) {
+        const u32x2_t v{uint32_t(__builtin_bit_cast(uint16_t, c[0])) | (uint32_t(__builtin_bit_cast(uint16_t, c[1])) << 16),
+                        uint32_t(__builtin_bit_cast(uint16_t, c[2])) | (uint32_t(__builtin_bit_cast(uint16_t, c[3])) << 16)};
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x2_t *>(dst));
+    } else {
+        const uint32_t v = uint32_t(uint8_t(c[0])) | (uint32_t(uint8_t(c[1])) << 8) |
+                           (uint32_t(uint8_t(c[2])) << 16) | (uint32_t(uint8_t(c[3])) << 24);
+        __builtin_nontemporal_store(v, reinterpret_cast<uint32_t *>(dst));
+    }
+}
+
+// A wave's output fragments straight into C with the epilogue EPI, four
+// consecutive outputs of a row per store.  Lane l holds,
 // for fragment (i, j) and register r, row r0 + 4 (l / 32) + 32 i + 8 (r / 4) + r % 4
-// and column c0 + l % 32 + 32 j: one base pointer per lane plus a row offset that
-// is a constant times ldc, which the scalar unit forms.  The epilogue is a template
-// argument so that the loop bodies stay small enough to unroll fully: the
-// accumulators are then only indexed by constants and stay in registers (with a
-// run-time choice per element, the 256-register tiles of the 4-wave 256 x 256
-// int8 kernels went to scratch).  The stores are non-temporal: C is written once
-// and not read back by the kernel, and streaming it past the caches keeps the A
-// and B panels that other workgroups are still reading resident in L2 and in the
-// last-level cache (measured at 8192^3: 6 % faster for int8, 3 % for bf16).
+// and column c0 + l % 32 + 32 j.  Each group of four registers (four consecutive
+// rows of one column) is transposed across the four lanes of a quad
+// (quad_transpose), after which lane l holds four consecutive columns,
+// c0 + 32 j + 4 ((l % 32) / 4) .. + 3, of row r0 + 4 (l / 32) + l % 4 + 32 i + 8 g,
+// and writes them with one store: a quarter of the store instructions of one
+// element per lane, which is what bounds the epilogue (each wave retires about one
+// store instruction per 80 clocks, whatever its width).  Where the four columns run
+// past N, or C's pitch or address does not allow the wide store, the four values go
+// out one by one.  Row offsets are constants times ldc, which the scalar unit forms.
+// The epilogue is a template argument so that the loop bodies stay small enough to
+// unroll fully: the accumulators are then only indexed by constants and stay in
+// registers (with a run-time choice per element, the 256-register tiles of the
+// 4-wave 256 x 256 int8 kernels went to scratch).  The stores are non-temporal: C
+// is written once and not read back by the kernel, and streaming it past the caches
+// keeps the A and B panels that other workgroups are still reading resident in L2
+// and in the last-level cache (measured at 8192^3: 6 % faster for int8, 3 % for
+// bf16).
 template <int DT, int EPI, int TM, int TN>
-__device__ __forceinline__ void store_c_direct(const KernelArgs &args,
+__device__ __forceinline__ void store_c_wide(const KernelArgs &args,
                                                const typename Types<DT>::acc_vec (&acc)[TM][TN],
                                                int64_t r0, int64_t c0, int lane) {
+    using o_t = typename OutElem<DT, EPI>::type;
+    using out_t = typename Types<DT>::out_t;
+    const int64_t row0 = r0 + 4 * (lane >> 5) + (lane & 3);
+    const int64_t col = c0 + (lane & 28);
+    const int64_t rows_left = args.M - row0;
+    const int64_t ldc = args.ldc;
+    const bool wide = (ldc % 4) == 0 && (reinterpret_cast<uintptr_t>(args.C) % (4 * sizeof(o_t))) == 0;
+    o_t *const base = static_cast<o_t *>(args.C) + row0 * ldc + col;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int64_t cols_left = args.N - (col + 32 * j);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                uint32_t x[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    // Copied out before the cast: clang's bit cast of a vector-element
+                    // expression reads the vector's first element, whatever the index.
+                    const auto e = acc[i][j][4 * g + k];
+                    x[k] = __builtin_bit_cast(uint32_t, e);
+                }
+                quad_transpose(x, lane);
+                o_t c[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) c[k] = convert_out<DT, EPI>(args, __builtin_bit_cast(out_t, x[k]));
+                const int dr = 32 * i + 8 * g;
+                if (dr < rows_left && cols_left > 0) {
+                    o_t *const dst = base + dr * ldc + 32 * j;
+                    if (wide && cols_left >= 4) {
+                        store4_nt(dst, c);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+                            if (k < cols_left) __builtin_nontemporal_store(c[k], dst + k);
+                    }
+                }
+            }
+            // One fragment at a time: keeps the scheduler from reading every accumulator
+            // out ahead of its stores.
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// The same, one output per store: lane l writes its registers as they are (column
+// c0 + l % 32 + 32 j, two rows per store instruction).  Kept for the 4-wave
+// 256 x 256 tiles, whose waves each hold a 128 x 128 block (256 accumulator
+// registers): the transposes' extra live values would push them into scratch.
+template <int DT, int EPI, int TM, int TN>
+__device__ __forceinline__ void store_c_elementwise(const KernelArgs &args,
+                                                    const typename Types<DT>::acc_vec (&acc)[TM][TN],
+                                                    int64_t r0, int64_t c0, int lane) {
     using o_t = typename OutElem<DT, EPI>::type;
     const int64_t row0 = r0 + 4 * (lane >> 5);
     const int64_t col = c0 + (lane & 31);
@@ -233,11 +336,22 @@ __device__ __forceinline__ void store_c_direct(const KernelArgs &args,
                 if (dr < rows_left)
                     __builtin_nontemporal_store(convert_out<DT, EPI>(args, acc[i][j][r]), &base[dr * ldc + 32 * j]);
             }
-            // One fragment at a time: keeps the scheduler from reading every accumulator
-            // out ahead of its stores.
             __builtin_amdgcn_sched_barrier(0);
         }
     }
+}
+
+// Which form a tile uses, as measured (same-process A/B against element-wise
+// stores): four-wave tiles of at most 64 x 64 per wave write a quarter of the
+// store instructions and gain (128 x 128 at 2048^3: 3.5 %); tiles of eight waves
+// lose 1-7 %, their epilogue being bound by the chip's aggregate write rate rather
+// than by store instructions, so the transposes only add VALU work.
+template <int DT, int EPI, int WAVES, int TM, int TN>
+__device__ __forceinline__ void store_c_direct(const KernelArgs &args,
+                                               const typename Types<DT>::acc_vec (&acc)[TM][TN],
+                                               int64_t r0, int64_t c0, int lane) {
+    if constexpr (WAVES <= 4 && TM * TN <= 4) store_c_wide<DT, EPI, TM, TN>(args, acc, r0, c0, lane);
+    else store_c_elementwise<DT, EPI, TM, TN>(args, acc, r0, c0, lane);
 }
 
 // s_last: one int of LDS for the in-kernel split-K reduction's "last slice"
@@ -251,18 +365,19 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
                                            int &s_last) {
     using out_t = typename Types<DT>::out_t;
     using sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;  // int32 wraps mod 2^32
+    constexpr int WAVES = (BM / (32 * TM)) * (BN / (32 * TN));
     const int frag_row = lane & 31, frag_half = lane >> 5;
     const int64_t M = args.M, N = args.N;
     const int64_t plane = M * N;
     if (args.split_k == 1) {
         // C itself, through the call's output conversion.
         if constexpr (DT == DT_I8) {
-            if (args.epilogue == EPI_I8) store_c_direct<DT, EPI_I8>(args, acc, r0, c0, lane);
-            else if (args.epilogue == EPI_I16) store_c_direct<DT, EPI_I16>(args, acc, r0, c0, lane);
-            else store_c_direct<DT, EPI_NONE>(args, acc, r0, c0, lane);
+            if (args.epilogue == EPI_I8) store_c_direct<DT, EPI_I8, WAVES>(args, acc, r0, c0, lane);
+            else if (args.epilogue == EPI_I16) store_c_direct<DT, EPI_I16, WAVES>(args, acc, r0, c0, lane);
+            else store_c_direct<DT, EPI_NONE, WAVES>(args, acc, r0, c0, lane);
         } else {
-            if (args.epilogue == EPI_BF16) store_c_direct<DT, EPI_BF16>(args, acc, r0, c0, lane);
-            else store_c_direct<DT, EPI_NONE>(args, acc, r0, c0, lane);
+            if (args.epilogue == EPI_BF16) store_c_direct<DT, EPI_BF16, WAVES>(args, acc, r0, c0, lane);
+            else store_c_direct<DT, EPI_NONE, WAVES>(args, acc, r0, c0, lane);
         }
         return;
     }
