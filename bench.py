@@ -42,6 +42,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (AMD published)
+REDUCE_NAMES = {0: "separate", 1: "last-slice", 2: "atomic"}   # split-K reductions (GEMM_REDUCE_*)
 HBM_GBS = 8000.0
 KERNEL_DIR = os.path.join(ROOT, "paper_2512_13282_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -279,6 +280,7 @@ def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
         "ms_per_step": round(ms_step, 5), "kernel_ms_avg": round(k_avg, 5), "kernel_ms_min": round(k_min, 5),
         "pct_dense_peak": round(100.0 * value / PEAK[w.dtype], 2),
         "plan": plan["name"], "split_k": plan["split_k"], "grid": plan["grid"],
+        "reduce": REDUCE_NAMES[plan["reduce_in_kernel"]] if plan["split_k"] > 1 else None,
         "algorithmic_ops_per_launch": ops, "algorithmic_bytes_per_launch": comp_bytes,
         "roofline": roof,
     }
@@ -388,7 +390,7 @@ def config_table(skip, steps: int, warmup: int):
         ops = 2.0 * M * N * K
         bare = bare_read_us(w) if skinny else None
         row = {"dtype": dtype, "M": M, "K": K, "N": N, "protocol": proto, "plan": r["plan"],
-               "split_k": r["split_k"], "kernel_us": round(kavg * 1e3, 2),
+               "split_k": r["split_k"], "reduce": r["reduce"], "kernel_us": round(kavg * 1e3, 2),
                "value": round(ops / (kavg * 1e-3) / 1e12, 2), "unit": r["unit"],
                "pct_dense_peak": round(100.0 * ops / (kavg * 1e-3) / 1e12 / PEAK[dtype], 2),
                "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac")},
@@ -400,7 +402,7 @@ def config_table(skip, steps: int, warmup: int):
         rows.append(row)
         print(f"[configs] {dtype:4s} M={M:5d} K={K:6d} N={N:6d} {row['kernel_us']:9.1f} us {row['value']:9.2f} "
               f"{row['unit']:7s} {row['roofline']['bound']} frac={row['roofline']['frac']:.3f} plan={row['plan']} "
-              f"x{row['split_k']} ok={row['parity_sample_ok']}"
+              f"x{row['split_k']}{' ' + row['reduce'] if row['reduce'] else ''} ok={row['parity_sample_ok']}"
               + (f" bare-read={row['bare_read_of_B_us']}us ({row['frac_of_bare_read']:.2f})" if "bare_read_of_B_us" in row else ""),
               file=sys.stderr, flush=True)
         del w

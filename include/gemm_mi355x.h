@@ -98,9 +98,12 @@ typedef struct gemm_plan_info {
     int32_t waves;           /* wavefronts per workgroup                       */
     int32_t mfma_m, mfma_n, mfma_k;  /* MFMA instruction shape (0: none, GEMV) */
     int32_t split_k;         /* K slices (1 = no split)                        */
-    int32_t reduce_in_kernel;/* split-K partials summed by the last slice of each
-                                tile inside the GEMM kernel (1) or by a second
-                                kernel (0); 0 when split_k == 1                */
+    int32_t reduce_in_kernel;/* split-K reduction, GEMM_REDUCE_*: partials summed
+                                by a second kernel (0), by the last slice of
+                                each tile inside the GEMM kernel (1), or added
+                                into C, zeroed first, with device atomics (2;
+                                int8 only; the narrowed-output calls of such a
+                                plan use 0); 0 when split_k == 1              */
     int64_t k_chunk;         /* K elements per slice                           */
     int64_t grid;            /* workgroups of the main kernel                  */
     int64_t lds_bytes;       /* LDS per workgroup                              */
@@ -112,11 +115,21 @@ typedef struct gemm_plan_info {
     char    name[48];        /* human-readable kernel/config name              */
 } gemm_plan_info;
 
+/* Split-K reductions (gemm_plan_info.reduce_in_kernel, gemm_force_reduce). */
+enum {
+    GEMM_REDUCE_SEPARATE = 0,   /* a second kernel sums the slices' partial planes      */
+    GEMM_REDUCE_LAST_SLICE = 1, /* the slice of each tile that finishes last sums them  */
+    GEMM_REDUCE_ATOMIC = 2      /* int8, int32 output: C zeroed, then every slice adds
+                                   its partial tile into C with device atomics          */
+};
+
 /* Test and benchmark hook: force the split-K reduction for every later call of
- * `dtype` (1 = in-kernel by the last slice of each tile, 0 = separate reduction
- * kernel, -1 = the selector's choice).  Both sum the K slices in the same fixed
- * order, so the result does not depend on this choice.  Not thread-safe with
- * respect to concurrent GEMM calls.  Returns GEMM_ERR_INVALID_VALUE for an
+ * `dtype` (a GEMM_REDUCE_* value, or -1 = the selector's choice).  The first two
+ * sum the K slices in the same fixed order, so fp32 results do not depend on the
+ * choice; the atomic one adds int32 partials in whatever order they arrive, which
+ * modulo 2^32 gives the same bits.  A bf16 plan asked for the atomic reduction
+ * uses the separate one, as do the int8 -> int8 / int16 calls.  Not thread-safe
+ * with respect to concurrent GEMM calls.  Returns GEMM_ERR_INVALID_VALUE for an
  * unknown dtype or mode. */
 int gemm_force_reduce(int dtype, int mode);
 

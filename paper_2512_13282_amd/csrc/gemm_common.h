@@ -115,12 +115,15 @@ __device__ __forceinline__ void map_tile(const KernelArgs &a, int &tm, int &tn, 
 //
 // With split-K each K slice stores its partial tile in the workspace
 // ([split][M][N]).  Then either a separate kernel sums the planes
-// (splitk_reduce_kernel), or, with args.reduce_in_kernel, every slice takes a
-// ticket from the tile's arrival counter and the workgroup that arrives last
-// sums the slices of the tile and writes C, then resets the counter to zero
+// (REDUCE_SEPARATE, splitk_reduce_kernel), or (REDUCE_LAST_SLICE) every slice
+// takes a ticket from the tile's arrival counter and the workgroup that arrives
+// last sums the slices of the tile and writes C, then resets the counter to zero
 // for the next launch on the stream.  Both sum in the fixed slice order
 // 0, 1, ..., so fp32 results are identical run to run whichever slice finishes
-// last and whichever reduction runs.
+// last and whichever reduction runs.  int8 with int32 output may instead add
+// every slice's partial tile straight into C, zeroed beforehand, with device
+// atomics (REDUCE_ATOMIC): integer addition is exact and order-free, so the bits
+// are the same, with no workspace and no second pass over partial planes.
 //
 // The slices of a tile run on different XCDs, whose L2 caches are not kept
 // coherent with each other for ordinary accesses.  Instead of device-scope
@@ -381,7 +384,28 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
         }
         return;
     }
-    if (!args.reduce_in_kernel) {
+    if constexpr (DT == DT_I8) {
+        if (args.reduce_in_kernel == REDUCE_ATOMIC) {
+            // Relaxed device-scope adds, no return value: the kernel's end orders them
+            // before anything that reads C.
+            uint32_t *const cc = static_cast<uint32_t *>(args.C);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const int64_t col = c0 + j * 32 + frag_row;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int64_t row = r0 + i * 32 + 8 * (r >> 2) + 4 * frag_half + (r & 3);
+                        if (row < M && col < N)
+                            __hip_atomic_fetch_add(&cc[row * args.ldc + col], uint32_t(acc[i][j][r]),
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                }
+            return;
+        }
+    }
+    if (args.reduce_in_kernel == REDUCE_SEPARATE) {
         // This slice's partial plane for the separate reduction.
         out_t *out = static_cast<out_t *>(args.workspace) + int64_t(slice) * plane;
 #pragma unroll

@@ -172,14 +172,31 @@ static int static_scratch_address(uint8_t **out) {
     return LAUNCH_OK;
 }
 
+// Zeroes the M x N outputs of an int32 C with row pitch ldc (the atomic split-K
+// reduction's starting point); the row padding is not touched.
+__global__ __launch_bounds__(256) void zero_c_kernel(uint32_t *__restrict__ c, int64_t M, int64_t N, int64_t ldc) {
+    const int64_t stride = int64_t(gridDim.x) * blockDim.x, total = M * N;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t r = i / N;
+        c[r * ldc + (i - r * N)] = 0u;
+    }
+}
+
 int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr, bool static_scratch) {
     hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
     KernelArgs args = a;
     args.workspace = nullptr;
     args.counters = nullptr;
-    if (args.split_k > 1) {
+    if (args.split_k > 1 && args.reduce_in_kernel == REDUCE_ATOMIC) {
+        if (args.dtype != DT_I8 || args.epilogue != EPI_NONE) return LAUNCH_HIP_ERROR;
+        int64_t blocks = (args.M * args.N + 255) / 256;
+        if (blocks > 2048) blocks = 2048;
+        hipLaunchKernelGGL(zero_c_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, static_cast<uint32_t *>(args.C),
+                           args.M, args.N, args.ldc);
+        if (hipGetLastError() != hipSuccess) return LAUNCH_HIP_ERROR;
+    } else if (args.split_k > 1) {
         const size_t bytes = size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
-        const int64_t tiles = args.reduce_in_kernel ? int64_t(args.tiles_m) * args.tiles_n : 0;
+        const int64_t tiles = args.reduce_in_kernel == REDUCE_LAST_SLICE ? int64_t(args.tiles_m) * args.tiles_n : 0;
         if (static_scratch) {
             if (bytes > size_t(kStaticScratchBytes - kScratchCounterBytes) || tiles * 4 > kScratchCounterBytes)
                 return LAUNCH_SCRATCH_LIMIT;
@@ -203,7 +220,7 @@ int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr
     }
     hipError_t e = args.dtype == DT_I8 ? launch_config<DT_I8>(cfg, args, grid, stream)
                                        : launch_config<DT_BF16>(cfg, args, grid, stream);
-    if (e == hipSuccess && args.split_k > 1 && !args.reduce_in_kernel) {
+    if (e == hipSuccess && args.split_k > 1 && args.reduce_in_kernel == REDUCE_SEPARATE) {
         const int64_t total = args.M * args.N;
         int64_t blocks = (total + 255) / 256;
         if (blocks > 8192) blocks = 8192;

@@ -202,7 +202,8 @@ using gemv_sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type
 // Writes `cols` results v[c] of columns n0 + c (one output row) for K slice
 // `slice`: straight into C without split-K, else into the slice's partial plane;
 // with the in-kernel reduction the workgroup arriving last for this column block
-// sums the planes in slice order.  Thread t handles c = t, t + 256, ...
+// sums the planes in slice order; with the atomic one (int8, int32 output) every
+// slice adds into C, zeroed beforehand.  Thread t handles c = t, t + 256, ...
 template <int DT, int COLS>
 __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_acc_t<DT> *v, int64_t n0,
                                            int tile, int slice) {
@@ -215,7 +216,16 @@ __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_ac
             if (n0 + c < N) write_c<DT>(args, n0 + c, v[c]);
         return;
     }
-    if (!args.reduce_in_kernel) {
+    if constexpr (DT == DT_I8) {
+        if (args.reduce_in_kernel == REDUCE_ATOMIC) {     // into C, zeroed beforehand
+            for (int c = t; c < COLS; c += 256)
+                if (n0 + c < N)
+                    __hip_atomic_fetch_add(&static_cast<uint32_t *>(args.C)[n0 + c], uint32_t(v[c]), __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+    }
+    if (args.reduce_in_kernel == REDUCE_SEPARATE) {
         for (int c = t; c < COLS; c += 256)
             if (n0 + c < N) ws[int64_t(slice) * N + n0 + c] = sum_t(v[c]);
         return;

@@ -19,7 +19,7 @@ struct KernelArgs {
     int32_t split_k;
     int32_t tiles_m, tiles_n;      // output tiles along M and N
     int32_t group_m;               // tile-rows per group in the launch order
-    int32_t reduce_in_kernel;      // split-K: 1 = last slice of each tile sums it, 0 = separate kernel
+    int32_t reduce_in_kernel;      // split-K reduction, REDUCE_* below
     int32_t b_trans;               // 1: B is stored column-major (N x K, row stride ldb >= K)
     int32_t epilogue;              // output conversion, EPI_* below
     int32_t shift;                 // EPI_I8 / EPI_I16: results are divided by 2^shift
@@ -30,6 +30,14 @@ struct KernelArgs {
 // to even, saturated to the int8 / int16 range.  EPI_BF16: fp32 result rounded
 // to the nearest bf16, ties to even.
 enum { EPI_NONE = 0, EPI_I8 = 1, EPI_I16 = 2, EPI_BF16 = 3 };
+
+// Split-K reductions.  REDUCE_SEPARATE: every slice writes its partial plane and a
+// second kernel sums the planes.  REDUCE_LAST_SLICE: the slice of each tile that
+// finishes last sums the tile's partials.  REDUCE_ATOMIC (int8 with int32 output
+// only): C is zeroed first and every slice adds its partial tile into C with device
+// atomics; int32 addition modulo 2^32 is exact and order-free, so the result is the
+// same bits as the other two give, and no workspace is needed.
+enum { REDUCE_SEPARATE = 0, REDUCE_LAST_SLICE = 1, REDUCE_ATOMIC = 2 };
 
 enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2, LAUNCH_SCRATCH_LIMIT = 3 };
 

@@ -15,6 +15,7 @@
 // never splitting K across cores (Sec. 4.2.1).  Split-K is therefore only
 // chosen where the tile count alone cannot fill the chip.
 #include "selector.h"
+#include "launch.h"
 
 #include <algorithm>
 #include <cmath>
@@ -68,7 +69,27 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
         pl.split_k = int32_t(ceil_div(p.K, pl.k_chunk));
     }
     pl.grid = pl.tiles_m * pl.tiles_n * pl.split_k;
-    pl.workspace_bytes = pl.split_k > 1 ? int64_t(pl.split_k) * p.M * p.N * 4 : 0;
+
+    // Split-K reduction (REDUCE_* in launch.h).  Last slice: the last slice of each
+    // tile reads the tile's partials, sixteen slices per round trip of 256 threads x 4
+    // columns, at the end of the kernel.  Separate: one more launch streaming the
+    // partial planes.  Atomic (int8 only, and only when asked for, by a measured plan
+    // or a forced mode): a fill launch ahead of the GEMM, the partial tiles added into
+    // C, no workspace.
+    double red_us = 0.0;
+    pl.reduce_in_kernel = REDUCE_SEPARATE;
+    if (pl.split_k > 1) {
+        const int64_t rows = std::min<int64_t>(c.bm, p.M), cols = std::min<int64_t>(c.bn, p.N);
+        const double trips = double(ceil_div(rows * ceil_div(cols, 4), 256)) * double(ceil_div(pl.split_k, 16));
+        const double in_kernel_us = trips * chip.round_trip_us;
+        const double separate_us = chip.launch_us;
+        int32_t mode = reduce >= 0 ? reduce : (in_kernel_us <= separate_us ? REDUCE_LAST_SLICE : REDUCE_SEPARATE);
+        if (mode == REDUCE_ATOMIC && p.dtype != DT_I8) mode = REDUCE_SEPARATE;
+        pl.reduce_in_kernel = mode;
+        red_us = mode == REDUCE_LAST_SLICE ? in_kernel_us : separate_us;
+    }
+    const bool partial_planes = pl.split_k > 1 && pl.reduce_in_kernel != REDUCE_ATOMIC;
+    pl.workspace_bytes = partial_planes ? int64_t(pl.split_k) * p.M * p.N * 4 : 0;
 
     // Compute: whole rounds of resident workgroups (wave quantization).
     const double ops_clk = p.dtype == DT_I8 ? chip.i8_ops_per_clk_cu : chip.bf16_ops_per_clk_cu;
@@ -81,30 +102,18 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
     pl.t_comp_us = double(rounds) * wg_s * 1e6;
 
     // Memory: compulsory traffic at HBM speed; tile re-reads (Eqs. 6-7 analog)
-    // mostly from L2/MALL; split-K partials written and read back once.
+    // mostly from L2/MALL; split-K partials written and read back once, or added
+    // into C once after C is zeroed.
     const double a_bytes = double(p.M) * p.K * e, b_bytes = double(p.K) * p.N * e;
     const double c_bytes = double(p.M) * p.N * 4;
     const double a_reads = a_bytes * double(pl.tiles_n);
     const double b_reads = b_bytes * double(pl.tiles_m);
-    const double ws = pl.split_k > 1 ? 2.0 * double(pl.workspace_bytes) : 0.0;
+    const double ws = partial_planes ? 2.0 * double(pl.workspace_bytes)
+                                     : (pl.split_k > 1 ? double(pl.split_k + 1) * p.M * p.N * 4 : 0.0);
     pl.traffic_bytes = a_reads + b_reads + c_bytes + ws;
     pl.t_mem_us = ((a_bytes + b_bytes + c_bytes + ws) / chip.hbm_bytes_per_s +
                    (a_reads + b_reads - a_bytes - b_bytes) / chip.reread_bytes_per_s) * 1e6;
 
-    // Split-K reduction.  In-kernel: the last slice of each tile reads the
-    // tile's partials, sixteen slices per round trip of 256 threads x 4
-    // columns, at the end of the kernel.  Separate: one more launch streaming
-    // the partial planes.
-    double red_us = 0.0;
-    pl.reduce_in_kernel = 0;
-    if (pl.split_k > 1) {
-        const int64_t rows = std::min<int64_t>(c.bm, p.M), cols = std::min<int64_t>(c.bn, p.N);
-        const double trips = double(ceil_div(rows * ceil_div(cols, 4), 256)) * double(ceil_div(pl.split_k, 16));
-        const double in_kernel_us = trips * chip.round_trip_us;
-        const double separate_us = chip.launch_us;
-        pl.reduce_in_kernel = reduce >= 0 ? reduce : (in_kernel_us <= separate_us ? 1 : 0);
-        red_us = pl.reduce_in_kernel ? in_kernel_us : separate_us;
-    }
     pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + chip.launch_us + red_us;
     return pl;
 }

@@ -18,8 +18,8 @@ struct Problem {
 struct Plan {
     int32_t config;      // index into kConfigs
     int32_t split_k;     // >= 1
-    int32_t reduce_in_kernel;  // split-K partials summed by the last slice of each tile (1) or by a
-                               // separate kernel (0)
+    int32_t reduce_in_kernel;  // split-K reduction: REDUCE_SEPARATE, REDUCE_LAST_SLICE or
+                               // REDUCE_ATOMIC (launch.h)
     int64_t k_chunk;     // K elements per slice (multiple of the stage depth)
     int64_t tiles_m, tiles_n;
     int64_t grid;

@@ -11,9 +11,10 @@ procedure of refining the modelled tile choice by measurement on the device
     python -m paper_2512_13282_amd.tune [--shapes default|FILE] [--out PATH] [--iters N]
 
 Every plan is first timed in a short burst (the median of --iters launches); the
-fastest --confirm plans are then re-timed over several interleaved rounds of 50
-launches after 30 untimed ones, the regime of a long run of GEMMs on a chip whose
-power manager has settled, and the choice is made on those times.
+fastest --confirm plans, plus the fastest of each split-K reduction, are then
+re-timed over several interleaved rounds of 50 launches after 30 untimed ones,
+the regime of a long run of GEMMs on a chip whose power manager has settled, and
+the choice is made on those times.
 
 Shapes default to the paper-shaped workload sweep (see inputs.py) with B
 row-major, plus the skinny and 8192^3 workloads with B stored column-major
@@ -142,7 +143,8 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
     try:
         for cfg in range(n_cfg):
             for split in (SPLITS_SMALL_M if M < 256 else SPLITS_LARGE):
-                for reduce in ((-1,) if split == 1 else (0, 1)):
+                reductions = (0, 1, 2) if dtype == "int8" else (0, 1)   # atomic: int8 only
+                for reduce in ((-1,) if split == 1 else reductions):
                     if b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, cfg, split) != 0:
                         continue
                     b.gemm_force_reduce(d, reduce)
@@ -164,6 +166,14 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
         # few are therefore timed again, interleaved over several rounds, after a warm-up long
         # enough for the power manager to settle, and the choice is made on those times.
         top = sorted(results, key=lambda r: r["us"])[:max(1, confirm)]
+        # The two regimes also rank the split-K reductions differently (the burst puts the
+        # atomic reduction's zeroing launch, which runs ahead of the GEMM, 1-2 us behind the
+        # separate reduction that it beats in sustained runs), so the fastest screened plan
+        # of every reduction is confirmed too.
+        for mode in sorted({r["reduce"] for r in results} - {-1}):
+            best_of_mode = min((r for r in results if r["reduce"] == mode), key=lambda r: r["us"])
+            if best_of_mode not in top:
+                top.append(best_of_mode)
         if len(top) > 1:
             times = [[] for _ in top]
             for _ in range(rounds):
@@ -187,7 +197,7 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
 def write_inc(entries, path=OUT):
     lines = ["// Generated by `python -m paper_2512_13282_amd.tune` from on-device measurements",
              "// (fastest plan per shape over sustained runs of back-to-back launches).  Fields: dtype, M, N, K, config, split_k, reduce,",
-             "// (split-K reduction: 1 in-kernel, 0 separate kernel, -1 the model's choice), B layout",
+             "// (split-K reduction: 0 separate kernel, 1 in-kernel by the last slice, 2 atomic adds into C, -1 the model's choice), B layout",
              "// (1: column-major).",
              "// Consulted by select_plan before the analytical model for an exact shape match."]
     for e in entries:

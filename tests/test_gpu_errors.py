@@ -1,6 +1,7 @@
 """Error paths of the C ABI that need a GPU: a split-K workspace that cannot be allocated
 returns GEMM_ERR_NO_MEMORY with nothing queued and C untouched, and the next call, with
-allocation possible again, runs normally (needs an MI355X)."""
+allocation possible again, runs normally; the atomic reduction, which needs no workspace,
+is unaffected (needs an MI355X)."""
 import numpy as np
 import pytest
 import torch
@@ -52,6 +53,19 @@ def test_workspace_failure_then_recovery(monkeypatch, config, split, reduce):
     assert g.bf16_error(Ab, Bb, Cb) <= g.BF16_TOL
     monkeypatch.delenv(HOOK)
     g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
+    rc, C = _call(b.gemm_i8_i32, A, B, -5)
+    assert rc == b.GEMM_OK, b.gemm_status_string(rc)
+    g.check_i8(A, B, C)
+
+
+def test_atomic_reduction_needs_no_workspace(monkeypatch):
+    """The atomic split-K reduction adds into C and allocates nothing: with every workspace
+    allocation failing it still runs, exactly."""
+    M, K, N = 64, 4096, 2048
+    A, B = inputs.make_inputs("int8", M, N, K, seed=11)
+    g.force(I8, b.GEMM_KERNEL_AUTO, 30, 8, b.GEMM_REDUCE_ATOMIC)
+    assert b.gemm_release_workspace() == b.GEMM_OK
+    monkeypatch.setenv(HOOK, "1")
     rc, C = _call(b.gemm_i8_i32, A, B, -5)
     assert rc == b.GEMM_OK, b.gemm_status_string(rc)
     g.check_i8(A, B, C)

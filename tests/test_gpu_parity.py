@@ -55,7 +55,7 @@ VEC_SHAPES = [(1, 16, 16), (37, 48, 48), (64, 256, 128), (300, 272, 1040), (257,
 ODD_SHAPES = [(1, 1, 1), (3, 5, 7), (17, 13, 31), (65, 63, 129), (129, 255, 257), (70, 300, 1001)]
 
 
-@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1)], ids=["s1", "s3sep", "s3fused"])
+@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1), (3, 2)], ids=["s1", "s3sep", "s3fused", "s3atomic"])
 @pytest.mark.parametrize("config", TILE_CONFIGS)
 @pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
 def test_every_config_matches_oracle(dtype, config, split, reduce):
@@ -187,8 +187,9 @@ def test_int8_split_k_is_invariant():
     A, B = _inputs(I8, M, N, K, seed=9)
     outs = []
     for split in (1, 2, 5, 16, 32):
-        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split)
-        outs.append(g.gemm_gpu(I8, A, B))
+        for reduce in (-1, b.GEMM_REDUCE_ATOMIC):
+            g.force(I8, b.GEMM_KERNEL_AUTO, 3, split, reduce)
+            outs.append(g.gemm_gpu(I8, A, B))
     for o in outs[1:]:
         assert np.array_equal(o, outs[0])
     g.check_i8(A, B, outs[0])
@@ -223,7 +224,7 @@ def test_split_k_workspace_reuse_across_shapes_and_streams():
         ref, _ = oracle.get().gemm_i8_i32(A, B)
         cases.append((M, N, K, A, B, ref))
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
-    for reduce in (1, 0):
+    for reduce in (1, 0, 2):
         for config, split in ((3, 6), (6, 16), (14, 5), (10, 3)):
             g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
             print(f"workspace reuse config={config} split={split} reduce={reduce}", flush=True)
@@ -243,6 +244,37 @@ def test_split_k_workspace_reuse_across_shapes_and_streams():
             for dA, dB, dC, ldc, M, N, ref in outs:
                 C = dC.cpu().numpy()[: M * ldc].reshape(M, ldc)[:, :N]
                 assert np.array_equal(C, ref), (config, split, reduce, M, N)
+
+
+@pytest.mark.parametrize("config,split,bt", [(28, 4, False), (31, 8, False), (30, 3, False), (14, 5, False),
+                                             (10, 2, True), (20, 7, True), (0, 3, False)])
+def test_int8_atomic_reduction(config, split, bt):
+    """Atomic split-K reduction: C's M x N outputs are zeroed and every slice adds its
+    partial tile into them.  Exact against the oracle on ragged shapes, the row padding
+    and the memory around C untouched, and a second call into the same (now non-zero) C
+    gives the same result."""
+    g.force(I8, b.GEMM_KERNEL_AUTO, config, split, b.GEMM_REDUCE_ATOMIC)
+    for M, N, K in [(75, 272, 2304), (1, 4112, 1024), (33, 48, 4096)]:
+        A, B = _inputs(I8, M, N, K, seed=60 + M)
+        Bx = np.ascontiguousarray(B.T) if bt else B
+        p = b.gemm_plan(I8, M, N, K, K, K if bt else N, N + 5, 1 << 40, 2 << 40, 3 << 40, trans_b=bt)
+        assert p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC and p["workspace_bytes"] == 0, p
+        dA, lda = g.to_dev(A)
+        dB, ldb = g.to_dev(Bx)
+        sentinel = -424242
+        dC, ldc = g.out_buffer(M, N, I8, pad_cols=5, sentinel=sentinel)
+        ref, ovf = oracle.get().gemm_i8_i32(A, B)
+        assert ovf == 0
+        for rep in range(2):
+            print(f"atomic reduce config={config} split={split} bt={bt} shape={(M, N, K)} rep={rep}", flush=True)
+            fn = g.call_bt if bt else g.call
+            assert fn(I8, M, N, K, dA, lda, dB, ldb, dC, ldc) == b.GEMM_OK
+            torch.cuda.synchronize()
+            host = dC.cpu().numpy()
+            C = host[: M * ldc].reshape(M, ldc)
+            assert np.array_equal(C[:, :N], ref), np.argwhere(C[:, :N] != ref)[:3].tolist()
+            assert (C[:, N:] == sentinel).all(), "row padding of C was written"
+            assert (host[M * ldc:] == sentinel).all(), "memory past C was written"
 
 
 def test_release_workspace_then_reuse():

@@ -51,7 +51,7 @@ VEC_SHAPES = [(1, 16, 16), (37, 45, 48), (64, 256, 128), (300, 270, 1040), (257,
 ODD_SHAPES = [(1, 1, 1), (3, 5, 7), (17, 13, 31), (65, 63, 129), (129, 255, 257), (70, 300, 1001)]
 
 
-@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1)], ids=["s1", "s3sep", "s3fused"])
+@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1), (3, 2)], ids=["s1", "s3sep", "s3fused", "s3atomic"])
 @pytest.mark.parametrize("config", BT_CONFIGS)
 @pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
 def test_every_bt_config_matches_oracle(dtype, config, split, reduce):

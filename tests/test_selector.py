@@ -30,7 +30,10 @@ def check_invariants(p, dtype, M, N, K):
         assert p["split_k"] * p["k_chunk"] >= K > (p["split_k"] - 1) * p["k_chunk"]
     else:
         assert p["split_k"] == 1
-    assert p["workspace_bytes"] == (p["split_k"] * M * N * 4 if p["split_k"] > 1 else 0)
+    planes = p["split_k"] > 1 and p["reduce_in_kernel"] != b.GEMM_REDUCE_ATOMIC
+    assert p["workspace_bytes"] == (p["split_k"] * M * N * 4 if planes else 0)
+    if p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC:
+        assert dtype == I8 and p["split_k"] > 1
     assert p["grid"] < 2 ** 31
 
 
@@ -171,6 +174,26 @@ def test_split_k_reduction_choice():
     finally:
         b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
         b.gemm_force_reduce(I8, -1)
+
+
+def test_atomic_reduction_plans():
+    """The atomic split-K reduction is int8-only and needs no workspace; asked of bf16, the
+    plan takes the separate reduction instead."""
+    try:
+        for d in (I8, BF):
+            assert b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, 28, 4) == b.GEMM_OK
+            assert b.gemm_force_reduce(d, b.GEMM_REDUCE_ATOMIC) == b.GEMM_OK
+        p = plan(I8, 16, 14336, 4096)
+        check_invariants(p, I8, 16, 14336, 4096)
+        assert p["split_k"] == 4 and p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC and p["workspace_bytes"] == 0
+        q = plan(BF, 16, 14336, 4096)
+        check_invariants(q, BF, 16, 14336, 4096)
+        assert q["split_k"] == 4 and q["reduce_in_kernel"] == b.GEMM_REDUCE_SEPARATE
+        assert q["workspace_bytes"] == 4 * 16 * 14336 * 4
+    finally:
+        for d in (I8, BF):
+            b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
+            b.gemm_force_reduce(d, -1)
 
 
 def plan_bt(dtype, M, N, K, ldbt=None, off=0):
