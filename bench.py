@@ -15,7 +15,9 @@ Default run (one GPU), in this order:
    same workload (`cpu_baseline`) and the timed output compared with every
    oracle row that sample computed (`parity_full`);
 3. the same two GEMMs with B stored column-major, and the sustained MFMA
-   ceiling of the chip.
+   ceiling of the chip (only the GEMM's MFMAs, no memory traffic): every
+   MFMA-bound row of `configs` also gets its fraction of that ceiling, the
+   clock-adjusted peak of the box it ran on.
 
 Prints ONE JSON line on stdout with a roofline object for the dominant kernel.
 
@@ -734,6 +736,16 @@ def main():
             print(f"[bench] {dtype} sustained MFMA ceiling (random operands, no memory traffic): "
                   f"{ceiling[dtype]['value']} at {ceiling[dtype]['clock_ghz']} GHz; GEMM kernel reaches "
                   f"{ceiling[dtype]['gemm_frac_of_ceiling']:.3f} of it", file=sys.stderr, flush=True)
+
+    if table is not None and ceiling:
+        # every MFMA-bound row against the same run's sustained MFMA rate: the clock-adjusted peak
+        for row in table:
+            c = ceiling.get(row["dtype"])
+            if c and row["roofline"]["bound"] == "mfma":
+                row["frac_of_mfma_ceiling"] = round(row["value"] / c["value"], 4)
+        print("[configs] fraction of the sustained MFMA ceiling: " +
+              ", ".join(f"{r['dtype']} {r['M']}x{r['K']}x{r['N']} {r['frac_of_mfma_ceiling']:.3f}"
+                        for r in table if "frac_of_mfma_ceiling" in r), file=sys.stderr, flush=True)
 
     head_dtype = args.only or "int8"
     hw, hr = results[head_dtype]
