@@ -7,7 +7,8 @@ Default run (one GPU), in this order:
    2048^3 / 4096^3 squares, the three rectangles, the twelve skinny shapes),
    each timed with HIP events on the launch stream under a labelled protocol
    (cold for the cache-sized and the memory-bound shapes, warm otherwise), with
-   its plan, roofline fraction and sampled oracle rows;
+   its plan, roofline fraction and sampled oracle rows, and the CPU oracle timed on
+   the first rows of the same workload (`cpu_oracle`, those rows also compared);
 2. the headline: the int8 -> int32 GEMM at M = N = K = 8192 (`value`, TOPS) and
    the bf16 -> fp32 GEMM at the same size (the `bf16` object), inputs resident
    in HBM, W untimed warm-up launches, then K timed launches bracketed by device
@@ -37,6 +38,7 @@ import json
 import os
 import sys
 import time
+import types
 
 import numpy as np
 
@@ -45,6 +47,7 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (AMD published)
 REDUCE_NAMES = {0: "separate", 1: "last-slice", 2: "atomic"}   # split-K reductions (GEMM_REDUCE_*)
+CONFIG_ORACLE_SECONDS = 0.25  # CPU oracle work per row of the workload table (`cpu_oracle`)
 HBM_GBS = 8000.0
 KERNEL_DIR = os.path.join(ROOT, "paper_2512_13282_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -361,7 +364,7 @@ def bare_read_us(w: Workload, steps: int = 50, warmup: int = 10) -> float:
     return e0.elapsed_time(e1) * 1e3 / steps
 
 
-def config_table(skip, steps: int, warmup: int):
+def config_table(skip, steps: int, warmup: int, oracle_seconds: float = 0.0):
     """Every workload of the sweep (inputs.ALL_CONFIGS) except those in `skip`, timed with
     HIP events on the launch stream.  Shapes whose operands fit in the caches (int8 256^3,
     bf16 1024^3) are timed cold, one launch at a time after a 512 MiB flush; the skinny
@@ -370,10 +373,13 @@ def config_table(skip, steps: int, warmup: int):
     a spin kernel and timed between two events, so that each is timed on the GPU rather than
     waiting on the host's next launch (a Python launch takes longer than the smallest kernels).
     Each row carries its
-    protocol, plan, roofline fraction and a parity check of sampled output rows."""
+    protocol, plan, roofline fraction and a parity check of sampled output rows; with
+    `oracle_seconds` > 0 also the CPU oracle timed on the first rows of the same workload
+    (about that many seconds of work, `cpu_oracle`) and those rows of the timed output compared
+    with it (`parity_oracle_rows`)."""
     import torch
     from paper_2512_13282_amd import inputs
-    rows = []
+    rows, pending = [], []
     for (dtype, M, K, N) in inputs.ALL_CONFIGS:
         if (dtype, M, K, N) in skip:
             continue
@@ -397,6 +403,11 @@ def config_table(skip, steps: int, warmup: int):
                "pct_dense_peak": round(100.0 * ops / (kavg * 1e-3) / 1e12 / PEAK[dtype], 2),
                "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac")},
                "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))}
+        if oracle_seconds > 0:
+            # the oracle runs after every row is timed: CPU work between rows would leave the
+            # GPU idle and let its clock drop before the next row's short warm-up
+            pending.append((row, types.SimpleNamespace(dtype=dtype, M=M, N=N, K=K, A_host=w.A_host,
+                                                       B_host=w.B_host, dC=w.dC.cpu())))
         if bare is not None:
             # a plain read of B under the same protocol (the GEMM also reads A and writes C)
             row["bare_read_of_B_us"] = round(bare, 2)
@@ -409,6 +420,13 @@ def config_table(skip, steps: int, warmup: int):
               file=sys.stderr, flush=True)
         del w
         torch.cuda.empty_cache()
+    for row, hw in pending:
+        cb = cpu_baseline(hw, oracle_seconds)
+        row["cpu_oracle"] = {k: cb[k] for k in ("value", "unit", "cores", "seconds", "sample")}
+        row["parity_oracle_rows"] = parity_full(hw)
+        print(f"[oracle] {row['dtype']:4s} M={row['M']:5d} K={row['K']:6d} N={row['N']:6d} "
+              f"{cb['value']} {cb['unit']} on {cb['cores']} threads ({cb['sample']}); timed output rows "
+              f"ok={row['parity_oracle_rows']['ok']}", file=sys.stderr, flush=True)
     return rows
 
 
@@ -647,7 +665,8 @@ def main():
     heads = [(d, S, S, S) for d in (["int8", "bf16"] if args.only is None else [args.only])]
     # The per-workload table runs first: besides its own figures, it brings the chip to the
     # clock it holds under sustained GEMM load before the headline's warm-up and timed launches.
-    table = None if args.no_configs else config_table(set(heads), args.config_steps, args.config_warmup)
+    table = None if args.no_configs else config_table(set(heads), args.config_steps, args.config_warmup,
+                                                      0.0 if args.no_cpu_baseline else CONFIG_ORACLE_SECONDS)
 
     results = {}
     for dtype in (["int8", "bf16"] if args.only is None else [args.only]):
