@@ -59,9 +59,12 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    # The chip's power management needs about 30 launches of the 8192^3 GEMM to settle: the
-    # first few run at a higher clock, the next twenty or so dip below the steady state.
+    # The chip's power management needs a few tens of milliseconds of a new load to settle on
+    # its sustained clock: launches timed within that window run up to 1.2x slower.  Every
+    # timed workload therefore first runs untimed for --settle-ms, then its W warm-up launches.
     ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--settle-ms", type=float, default=SETTLE_MS,
+                    help="untimed launches of each workload for this long before its warm-up (0: none)")
     ap.add_argument("--size", type=int, default=8192)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -196,12 +199,32 @@ def spin_ahead(launches: int, host_us_per_launch: float = 80.0) -> None:
     torch.cuda._sleep(int(_SPIN_RATE * host_us_per_launch * launches))
 
 
-def time_back_to_back(w: Workload, steps: int, warmup: int):
+SETTLE_MS = 100.0   # untimed launches ahead of every timed workload (--settle-ms)
+
+
+def settle(w: Workload, ms: float) -> None:
+    """Untimed launches of the workload for at least `ms` of wall time.  The chip's power
+    manager needs that long to settle on the clock it sustains under a new load: timed launches
+    that start within a few tens of milliseconds of an idle or lighter phase (a fresh process,
+    the CPU oracle, the previous workload) run up to 1.2x slower than the same launches a
+    moment later."""
+    import torch
+    if ms <= 0:
+        return
+    end = time.perf_counter() + ms / 1e3
+    while time.perf_counter() < end:
+        for _ in range(8):
+            w.launch()
+        torch.cuda.synchronize()
+
+
+def time_back_to_back(w: Workload, steps: int, warmup: int, settle_ms: float = SETTLE_MS):
     """W untimed launches; then, behind a spin kernel that lets the host queue them all,
     `steps` back-to-back launches between two HIP events on the launch stream.  Returns the
     GPU time per launch in ms (kernel plus the GPU's own gap between kernels; events around
     every launch would add their own overhead, a few microseconds per launch)."""
     import torch
+    settle(w, settle_ms)
     for _ in range(warmup):
         w.launch()
     torch.cuda.synchronize()
@@ -216,10 +239,11 @@ def time_back_to_back(w: Workload, steps: int, warmup: int):
     return ms, ms, ms
 
 
-def time_workload(w: Workload, steps: int, warmup: int):
-    """W untimed launches, then `steps` launches with HIP events on the launch stream around
-    each.  Returns (wall ms per step, mean kernel ms, min kernel ms)."""
+def time_workload(w: Workload, steps: int, warmup: int, settle_ms: float = SETTLE_MS):
+    """The settle phase, W untimed launches, then `steps` launches with HIP events on the
+    launch stream around each.  Returns (wall ms per step, mean kernel ms, min kernel ms)."""
     import torch
+    settle(w, settle_ms)
     for _ in range(warmup):
         w.launch()
     torch.cuda.synchronize()
@@ -239,12 +263,13 @@ def time_workload(w: Workload, steps: int, warmup: int):
 FLUSH_BYTES = 512 * 1024 * 1024      # twice the last-level cache
 
 
-def time_workload_flushed(w: Workload, steps: int, warmup: int):
+def time_workload_flushed(w: Workload, steps: int, warmup: int, settle_ms: float = SETTLE_MS):
     """Cold-cache timing for operands that fit in the caches: before every launch a 512 MiB
     scratch buffer is written (evicting A, B and C from the L2s and the 256 MB last-level
     cache), then the launch alone is timed with HIP events on the launch stream."""
     import torch
     scratch = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    settle(w, settle_ms)
     for _ in range(warmup):
         w.launch()
     torch.cuda.synchronize()
@@ -364,7 +389,7 @@ def bare_read_us(w: Workload, steps: int = 50, warmup: int = 10) -> float:
     return e0.elapsed_time(e1) * 1e3 / steps
 
 
-def config_table(skip, steps: int, warmup: int, oracle_seconds: float = 0.0):
+def config_table(skip, steps: int, warmup: int, oracle_seconds: float = 0.0, settle_ms: float = SETTLE_MS):
     """Every workload of the sweep (inputs.ALL_CONFIGS) except those in `skip`, timed with
     HIP events on the launch stream.  Shapes whose operands fit in the caches (int8 256^3,
     bf16 1024^3) are timed cold, one launch at a time after a 512 MiB flush; the skinny
@@ -388,10 +413,10 @@ def config_table(skip, steps: int, warmup: int, oracle_seconds: float = 0.0):
         copies = max(1, int(np.ceil(512e6 / (K * N * e))) + 1) if skinny else 1
         w = Workload(dtype, M, N, K, copies=copies)
         if (dtype, M, K, N) in inputs.SMALL:
-            ms, kavg, kmin = time_workload_flushed(w, steps, warmup)
+            ms, kavg, kmin = time_workload_flushed(w, steps, warmup, settle_ms)
             proto = "cold: 512 MiB flush before each launch, launches timed one by one"
         else:
-            ms, kavg, kmin = time_back_to_back(w, steps, warmup)
+            ms, kavg, kmin = time_back_to_back(w, steps, warmup, settle_ms)
             proto = (f"cold: back to back, B rotated over {copies} copies (> 512 MB between reuses)"
                      if skinny else "warm: back to back, operands resident")
         r = summarize(w, ms, kavg, kmin)
@@ -654,7 +679,7 @@ def main():
         dtype, shape = args.workload.split(":")
         M, K, N = (int(x) for x in shape.split("x"))
         w = Workload(dtype, M, N, K)
-        ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+        ms, kavg, kmin = time_workload(w, args.steps, args.warmup, args.settle_ms)
         r = summarize(w, ms, kavg, kmin)
         r.update({"workload": args.workload, "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))})
         print(json.dumps(r), flush=True)
@@ -666,12 +691,13 @@ def main():
     # The per-workload table runs first: besides its own figures, it brings the chip to the
     # clock it holds under sustained GEMM load before the headline's warm-up and timed launches.
     table = None if args.no_configs else config_table(set(heads), args.config_steps, args.config_warmup,
-                                                      0.0 if args.no_cpu_baseline else CONFIG_ORACLE_SECONDS)
+                                                      0.0 if args.no_cpu_baseline else CONFIG_ORACLE_SECONDS,
+                                                      args.settle_ms)
 
     results = {}
     for dtype in (["int8", "bf16"] if args.only is None else [args.only]):
         w = Workload(dtype, S, S, S)
-        ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+        ms, kavg, kmin = time_workload(w, args.steps, args.warmup, args.settle_ms)
         r = summarize(w, ms, kavg, kmin)
         r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
         if not args.no_cpu_baseline:
@@ -687,7 +713,7 @@ def main():
     if not args.no_bt:
         for dtype in (["int8", "bf16"] if args.only is None else [args.only]):
             w = Workload(dtype, S, S, S, bt=True)
-            ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+            ms, kavg, kmin = time_workload(w, args.steps, args.warmup, args.settle_ms)
             r = summarize(w, ms, kavg, kmin)
             r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
             bt_results[dtype] = {k: r[k] for k in ("value", "unit", "ms_per_step", "kernel_ms_avg",
@@ -703,7 +729,7 @@ def main():
             if args.only is not None and args.only != dtype:
                 continue
             w = Workload(dtype, S, S, S, out=out)
-            ms, kavg, kmin = time_workload(w, args.steps, args.warmup)
+            ms, kavg, kmin = time_workload(w, args.steps, args.warmup, args.settle_ms)
             r = summarize(w, ms, kavg, kmin)
             r["parity_sample_ok"] = parity_sample(w, [0, S // 2, S - 1])
             key = "int8_to_int8" if dtype == "int8" else "bf16_to_bf16"
@@ -734,7 +760,7 @@ def main():
                 bbytes = K * N * e
                 copies = 1 if M >= 256 else max(1, int(np.ceil(512e6 / bbytes)) + 1)
                 w = Workload(dtype, M, N, K, copies=copies)
-                ms, kavg, kmin = time_workload(w, max(20, args.steps // 2), args.warmup)
+                ms, kavg, kmin = time_workload(w, max(20, args.steps // 2), args.warmup, args.settle_ms)
                 r = summarize(w, ms, kavg, kmin)
                 r.update({"dtype": dtype, "M": M, "K": K, "N": N, "b_copies": copies})
                 r["parity_sample_ok"] = parity_sample(w, sorted({0, M - 1}))
@@ -772,7 +798,8 @@ def main():
         "metric": f"GEMM {'TOPS int8->int32' if head_dtype == 'int8' else 'TFLOP/s bf16->fp32'} "
                   f"M=N=K={S} on 1 MI355X (% of dense MFMA peak in pct_dense_peak)",
         "value": hr["value"], "unit": hr["unit"], "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": hr["ms_per_step"], "higher_is_better": True,
+        "warmup": args.warmup, "settle_ms": args.settle_ms, "ms_per_step": hr["ms_per_step"],
+        "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "i8" if head_dtype == "int8" else "bf16",
         "data": "synthetic: A, B seeded (PCG64 seed 0 / 1); int8 uniform [-128,127], bf16 N(0,1) rounded RNE",
