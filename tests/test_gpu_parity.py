@@ -325,17 +325,39 @@ def test_int8_extremes_largest_k(config):
     assert (C[:, ::2] == -16256 * K).all() and (C[:, 1::2] == 234881024).all()
 
 
+SPLIT_REDUCTIONS = [(1, -1), (4, b.GEMM_REDUCE_SEPARATE), (4, b.GEMM_REDUCE_LAST_SLICE), (4, b.GEMM_REDUCE_ATOMIC),
+                    (2, b.GEMM_REDUCE_ATOMIC)]
+
+
 def test_int8_wraps_past_int32():
-    """K = 131072 of (-128)(-128) = 2^31: documented to wrap modulo 2^32, like the oracle."""
+    """K = 131072 of (-128)(-128) = 2^31: documented to wrap modulo 2^32, like the oracle, with
+    every split-K reduction."""
     M, N, K = 32, 64, 131072
     A = np.full((M, K), -128, np.int8)
     B = np.full((K, N), -128, np.int8)
-    for split in (1, 4):
-        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split)
+    ref, ovf = oracle.get().gemm_i8_i32(A[:1], B[:, :1])
+    assert ovf == 1
+    for split, reduce in SPLIT_REDUCTIONS:
+        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split, reduce)
         C = g.gemm_gpu(I8, A, B)
-        ref, ovf = oracle.get().gemm_i8_i32(A[:1], B[:, :1])
-        assert ovf == 1
-        assert (C == ref[0, 0]).all(), (split, np.unique(C)[:4])
+        assert (C == ref[0, 0]).all(), (split, reduce, np.unique(C)[:4])
+
+
+def test_int8_partials_wrap_total_fits():
+    """K = 262144: the first half of the products are (-128)(-128), the second (127)(-128).
+    The running sum passes 2^31 halfway (a one-slice accumulator and the first slice's
+    partial wrap) and the total, 131072 * 128 = 2^24, fits: modulo-2^32 arithmetic must still
+    give it exactly, with every split and reduction."""
+    M, N, K = 32, 64, 262144
+    A = np.full((M, K), -128, np.int8)
+    A[:, K // 2:] = 127
+    B = np.full((K, N), -128, np.int8)
+    ref, ovf = oracle.get().gemm_i8_i32(A[:1], B[:, :1])
+    assert ovf == 0 and int(ref[0, 0]) == 2 ** 24
+    for split, reduce in SPLIT_REDUCTIONS:
+        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split, reduce)
+        C = g.gemm_gpu(I8, A, B)
+        assert (C == 2 ** 24).all(), (split, reduce, np.unique(C)[:4])
 
 
 def test_torch_helpers():
