@@ -73,9 +73,10 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
     // Split-K reduction (REDUCE_* in launch.h).  Last slice: the last slice of each
     // tile reads the tile's partials, sixteen slices per round trip of 256 threads x 4
     // columns, at the end of the kernel.  Separate: one more launch streaming the
-    // partial planes.  Atomic (int8 only, and only when asked for, by a measured plan
-    // or a forced mode): a fill launch ahead of the GEMM, the partial tiles added into
-    // C, no workspace.
+    // partial planes.  Atomic (int8 only): a fill launch ahead of the GEMM, the partial
+    // tiles added into C, no workspace; the model's choice for int8, where it costs the
+    // separate reduction's one extra launch without its partial planes (measured on the
+    // skinny shapes: it matches or beats both others).
     double red_us = 0.0;
     pl.reduce_in_kernel = REDUCE_SEPARATE;
     if (pl.split_k > 1) {
@@ -83,10 +84,12 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
         const double trips = double(ceil_div(rows * ceil_div(cols, 4), 256)) * double(ceil_div(pl.split_k, 16));
         const double in_kernel_us = trips * chip.round_trip_us;
         const double separate_us = chip.launch_us;
-        int32_t mode = reduce >= 0 ? reduce : (in_kernel_us <= separate_us ? REDUCE_LAST_SLICE : REDUCE_SEPARATE);
+        int32_t mode = reduce >= 0 ? reduce
+                     : p.dtype == DT_I8 ? REDUCE_ATOMIC
+                     : (in_kernel_us <= separate_us ? REDUCE_LAST_SLICE : REDUCE_SEPARATE);
         if (mode == REDUCE_ATOMIC && p.dtype != DT_I8) mode = REDUCE_SEPARATE;
         pl.reduce_in_kernel = mode;
-        red_us = mode == REDUCE_LAST_SLICE ? in_kernel_us : separate_us;
+        red_us = mode == REDUCE_LAST_SLICE ? in_kernel_us : separate_us;   // atomic: the fill launch
     }
     const bool partial_planes = pl.split_k > 1 && pl.reduce_in_kernel != REDUCE_ATOMIC;
     pl.workspace_bytes = partial_planes ? int64_t(pl.split_k) * p.M * p.N * 4 : 0;

@@ -156,24 +156,30 @@ def test_tuned_plans_skip_misaligned_operands():
 
 
 def test_split_k_reduction_choice():
-    """A small per-tile reduction (one row of output) is summed in the GEMM kernel by the last
-    slice; a large one (many rows times many slices) by the separate kernel; forcing either
-    is reflected in the plan, and split_k == 1 reports neither."""
+    """bf16: a small per-tile reduction (one row of output) is summed in the GEMM kernel by the
+    last slice, a large one (many rows times many slices) by the separate kernel.  int8: the
+    atomic reduction, whatever the size.  Forcing a reduction is reflected in the plan, and
+    split_k == 1 reports none."""
     try:
-        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 14, 16) == b.GEMM_OK
-        small = plan(I8, 1, 4096, 14336)
-        assert small["split_k"] == 16 and small["reduce_in_kernel"] == 1
-        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 3, 32) == b.GEMM_OK
-        large = plan(I8, 128, 4096, 16384)
-        assert large["split_k"] == 32 and large["reduce_in_kernel"] == 0
-        for mode in (0, 1):
+        for d in (I8, BF):
+            assert b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, 14, 16) == b.GEMM_OK
+        small = plan(BF, 1, 4096, 14336)
+        assert small["split_k"] == 16 and small["reduce_in_kernel"] == b.GEMM_REDUCE_LAST_SLICE
+        assert plan(I8, 1, 4096, 14336)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC
+        for d in (I8, BF):
+            assert b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, 3, 32) == b.GEMM_OK
+        large = plan(BF, 128, 4096, 16384)
+        assert large["split_k"] == 32 and large["reduce_in_kernel"] == b.GEMM_REDUCE_SEPARATE
+        assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC
+        for mode in (b.GEMM_REDUCE_SEPARATE, b.GEMM_REDUCE_LAST_SLICE, b.GEMM_REDUCE_ATOMIC):
             assert b.gemm_force_reduce(I8, mode) == b.GEMM_OK
             assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == mode
         assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 3, 1) == b.GEMM_OK
         assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == 0
     finally:
-        b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
-        b.gemm_force_reduce(I8, -1)
+        for d in (I8, BF):
+            b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
+            b.gemm_force_reduce(d, -1)
 
 
 def test_atomic_reduction_plans():
