@@ -261,6 +261,21 @@ __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_ac
     if (t == 0) __hip_atomic_store(&args.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// 4 x 4 byte transpose: col[j] gets byte j of r0, r1, r2, r3 (in that order, low byte
+// first).  Two rounds of byte permutes (v_perm_b32 picks bytes 0-3 from its second source
+// and 4-7 from its first): pair rows 0/1 and 2/3 by even and odd byte, then merge.
+__device__ __forceinline__ void transpose4x4_bytes(uint32_t r0, uint32_t r1, uint32_t r2, uint32_t r3,
+                                                   uint32_t (&col)[4]) {
+    const uint32_t t0 = __builtin_amdgcn_perm(r1, r0, 0x06020400u);   // r0.b0 r1.b0 r0.b2 r1.b2
+    const uint32_t t1 = __builtin_amdgcn_perm(r1, r0, 0x07030501u);   // r0.b1 r1.b1 r0.b3 r1.b3
+    const uint32_t t2 = __builtin_amdgcn_perm(r3, r2, 0x06020400u);
+    const uint32_t t3 = __builtin_amdgcn_perm(r3, r2, 0x07030501u);
+    col[0] = __builtin_amdgcn_perm(t2, t0, 0x05040100u);
+    col[1] = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
+    col[2] = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
+    col[3] = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
     using acc_t = gemv_acc_t<DT>;
@@ -320,23 +335,38 @@ __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
         }
     };
     auto use_batch = [&](const Batch &bt) {
+        if constexpr (DT == DT_I8) {
+            // Four rows at a time: each dword of the four rows' pieces (4 columns x 4 rows of
+            // bytes) is transposed so that a dword holds one column's four bytes, then one
+            // 4-way dot product with the four rows' A values adds them to that column.
+            static_assert(U % 4 == 0 && PIECES == 1, "int8 rows come in groups of four");
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int h = 0; h < PIECES; ++h)
+            for (int g = 0; g < U / 4; ++g) {
+                const uint32_t ap = (uint32_t(bt.a[4 * g]) & 0xFFu) | ((uint32_t(bt.a[4 * g + 1]) & 0xFFu) << 8) |
+                                    ((uint32_t(bt.a[4 * g + 2]) & 0xFFu) << 16) | (uint32_t(bt.a[4 * g + 3]) << 24);
 #pragma unroll
                 for (int w = 0; w < 4; ++w) {
-                    const unsigned x = bt.v[u][h][w];
-                    if constexpr (DT == DT_I8) {
+                    uint32_t col[4];
+                    transpose4x4_bytes(bt.v[4 * g][0][w], bt.v[4 * g + 1][0][w], bt.v[4 * g + 2][0][w],
+                                       bt.v[4 * g + 3][0][w], col);
 #pragma unroll
-                        for (int b = 0; b < 4; ++b)
-                            acc[4 * w + b] += int32_t(int8_t(uint8_t(x >> (8 * b)))) * bt.a[u];
-                    } else {
+                    for (int j = 0; j < 4; ++j)
+                        acc[4 * w + j] = __builtin_amdgcn_sdot4(int(col[j]), int(ap), acc[4 * w + j], false);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int h = 0; h < PIECES; ++h)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const unsigned x = bt.v[u][h][w];
                         acc[8 * h + 2 * w] = fmaf(__uint_as_float(x << 16), bt.a[u], acc[8 * h + 2 * w]);
                         acc[8 * h + 2 * w + 1] =
                             fmaf(__uint_as_float(x & 0xffff0000u), bt.a[u], acc[8 * h + 2 * w + 1]);
                     }
-                }
+        }
     };
     constexpr int64_t STEP = 4 * U;            // rows advanced per batch (four waves interleaved)
     Batch b0, b1;
