@@ -37,7 +37,7 @@ import numpy as np
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 OUT = os.path.join(PKG, "csrc", "tuned_plans.inc")
-SPLITS_SMALL_M = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
+SPLITS_SMALL_M = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64, 96, 128)
 SPLITS_LARGE = (1, 2, 3, 4)
 
 
@@ -137,6 +137,7 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
             raise RuntimeError(b.gemm_status_string(rc))
 
     results = []
+    measured = set()
     n_cfg = 0
     while b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, n_cfg, 0) == 0:
         n_cfg += 1
@@ -155,8 +156,10 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
                         continue            # configuration cannot run this shape
                     if plan["kernel"] == b.GEMM_KERNEL_GENERIC:
                         continue
-                    if plan["split_k"] != split and split != 1:
-                        continue            # clamped duplicate
+                    key = (cfg, plan["split_k"], plan["reduce_in_kernel"] if plan["split_k"] > 1 else -1)
+                    if key in measured:
+                        continue            # the split clamped to one already measured
+                    measured.add(key)
                     us = _time_flushed(run, iters) if cold_single else _time(run, copies, iters)
                     results.append({"config": cfg, "split": plan["split_k"],
                                     "reduce": plan["reduce_in_kernel"] if plan["split_k"] > 1 else -1,
