@@ -46,7 +46,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (AMD published)
-REDUCE_NAMES = {0: "separate", 1: "last-slice", 2: "atomic"}   # split-K reductions (GEMM_REDUCE_*)
+REDUCE_NAMES = {0: "separate", 1: "last-slice", 2: "atomic", 3: "atomic-flag"}   # split-K reductions (GEMM_REDUCE_*)
 CONFIG_ORACLE_SECONDS = 0.25  # CPU oracle work per row of the workload table (`cpu_oracle`)
 HBM_GBS = 8000.0
 KERNEL_DIR = os.path.join(ROOT, "paper_2512_13282_amd", "csrc")

@@ -101,9 +101,11 @@ typedef struct gemm_plan_info {
     int32_t reduce_in_kernel;/* split-K reduction, GEMM_REDUCE_*: partials summed
                                 by a second kernel (0), by the last slice of
                                 each tile inside the GEMM kernel (1), or added
-                                into C, zeroed first, with device atomics (2;
-                                int8 only; the narrowed-output calls of such a
-                                plan use 0); 0 when split_k == 1              */
+                                into C with device atomics, C zeroed by a fill
+                                kernel first (2) or by each tile's first slice
+                                inside the GEMM kernel (3) (2 and 3: int8 only;
+                                the narrowed-output calls of such a plan use 0);
+                                0 when split_k == 1                           */
     int64_t k_chunk;         /* K elements per slice                           */
     int64_t grid;            /* workgroups of the main kernel                  */
     int64_t lds_bytes;       /* LDS per workgroup                              */
@@ -119,15 +121,18 @@ typedef struct gemm_plan_info {
 enum {
     GEMM_REDUCE_SEPARATE = 0,   /* a second kernel sums the slices' partial planes      */
     GEMM_REDUCE_LAST_SLICE = 1, /* the slice of each tile that finishes last sums them  */
-    GEMM_REDUCE_ATOMIC = 2      /* int8, int32 output: C zeroed, then every slice adds
+    GEMM_REDUCE_ATOMIC = 2,     /* int8, int32 output: C zeroed, then every slice adds
                                    its partial tile into C with device atomics          */
+    GEMM_REDUCE_ATOMIC_FLAG = 3 /* as 2, but no fill kernel: the first K slice of each
+                                   tile zeroes it, and the others wait for its signal
+                                   before adding (RING and GEMV kernels; others use 2) */
 };
 
 /* Test and benchmark hook: force the split-K reduction for every later call of
  * `dtype` (a GEMM_REDUCE_* value, or -1 = the selector's choice).  The first two
  * sum the K slices in the same fixed order, so fp32 results do not depend on the
  * choice; the atomic one adds int32 partials in whatever order they arrive, which
- * modulo 2^32 gives the same bits.  A bf16 plan asked for the atomic reduction
+ * modulo 2^32 gives the same bits.  A bf16 plan asked for an atomic reduction
  * uses the separate one, as do the int8 -> int8 / int16 calls.  Not thread-safe
  * with respect to concurrent GEMM calls.  Returns GEMM_ERR_INVALID_VALUE for an
  * unknown dtype or mode. */

@@ -44,6 +44,7 @@ GEMM_KERNEL_GEMV = 5
 GEMM_REDUCE_SEPARATE = 0
 GEMM_REDUCE_LAST_SLICE = 1
 GEMM_REDUCE_ATOMIC = 2
+GEMM_REDUCE_ATOMIC_FLAG = 3
 
 EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt",
             "gemm_i8_i8", "gemm_i8_i16", "gemm_bf16_bf16", "gemm_i8_i8_bt", "gemm_i8_i16_bt",

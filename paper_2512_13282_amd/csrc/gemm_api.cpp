@@ -146,8 +146,10 @@ int run(int32_t dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K, const v
     a.tiles_n = int32_t(pl.tiles_n);
     a.group_m = 4;
     a.reduce_in_kernel = pl.reduce_in_kernel;
-    // The atomic reduction adds int32 partials into C: narrowed outputs take the separate one.
-    if (a.reduce_in_kernel == gemm::REDUCE_ATOMIC && epilogue != gemm::EPI_NONE) a.reduce_in_kernel = gemm::REDUCE_SEPARATE;
+    // The atomic reductions add int32 partials into C: narrowed outputs take the separate one.
+    if ((a.reduce_in_kernel == gemm::REDUCE_ATOMIC || a.reduce_in_kernel == gemm::REDUCE_ATOMIC_FLAG) &&
+        epilogue != gemm::EPI_NONE)
+        a.reduce_in_kernel = gemm::REDUCE_SEPARATE;
     a.b_trans = trans_b;
     a.epilogue = epilogue;
     a.shift = shift;
@@ -292,7 +294,7 @@ int gemm_force_plan(int dtype, int kernel, int config, int split_k) {
 
 int gemm_force_reduce(int dtype, int mode) {
     if (dtype != GEMM_DTYPE_I8_I32 && dtype != GEMM_DTYPE_BF16_F32) return GEMM_ERR_INVALID_VALUE;
-    if (mode < -1 || mode > 2) return GEMM_ERR_INVALID_VALUE;
+    if (mode < -1 || mode > 3) return GEMM_ERR_INVALID_VALUE;
     std::lock_guard<std::mutex> lk(g_mu);
     g_override[dtype].reduce = mode;
     return GEMM_OK;

@@ -147,6 +147,53 @@ __device__ __forceinline__ T load_coherent(const T *p) {
     return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// REDUCE_ATOMIC_FLAG.  Slice 0 of a tile zeroes the tile's part of C with
+// device-coherent stores before it loads anything, waits until every thread's zeros
+// are complete, and then adds split_k - 1 credits to the tile's counter.  Every other
+// slice reads the counter some K steps before its end (early, so that the read's
+// latency hides under the last steps), polls only if no credit had arrived by then,
+// gives one credit back and then adds its partial tile into C.  So a slice adds only
+// after the zeros of its tile are complete at the coherence point, where the atomics
+// are performed, and the counter is zero again when the launch ends.  A waiting
+// slice depends only on slice 0 of its tile, which waits for nothing; on every XCD
+// the slice-0 workgroups have the lowest numbers (map_tile) and start first.  The
+// polling is bounded all the same (about a second), so a slice 0 that never runs
+// cannot hang the kernel; its tile's result is then wrong.
+constexpr unsigned kCreditPollLimit = 1u << 20;
+
+// Slice 0's part, by all NT threads of the workgroup: the BM x BN tile at (m0, n0),
+// clipped to M x N.
+template <int BM, int BN, int NT>
+__device__ __forceinline__ void flag_zero_tile(const KernelArgs &args, int64_t m0, int64_t n0, int tile) {
+    uint32_t *const cc = static_cast<uint32_t *>(args.C);
+    const int rows = int((args.M - m0) < BM ? (args.M - m0) : BM);
+    const int cols = int((args.N - n0) < BN ? (args.N - n0) : BN);
+    for (int e = int(threadIdx.x); e < rows * BN; e += NT) {
+        const int r = e / BN, c = e % BN;
+        if (c < cols) store_coherent(&cc[(m0 + r) * args.ldc + n0 + c], 0u);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's zeros are complete
+    __syncthreads();                                   // ... and every thread's
+    if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(&args.counters[tile], uint32_t(args.split_k - 1), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Another slice's part, by every thread before its atomics; `seen` is the counter as
+// thread 0 read it earlier (0 if it did not).
+__device__ __forceinline__ void flag_take_credit(const KernelArgs &args, int tile, uint32_t seen) {
+    if (threadIdx.x == 0) {
+        uint32_t v = seen;
+        for (unsigned i = 0; v == 0u && i < kCreditPollLimit; ++i) {
+            __builtin_amdgcn_s_sleep(8);
+            v = load_coherent(&args.counters[tile]);
+        }
+        if (v != 0u)
+            __hip_atomic_fetch_sub(&args.counters[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+}
+
 // Output element idx (row * ldc + col, in output elements) of C from a result v of
 // the accumulator type, converted as the call's epilogue asks (launch.h).  int32
 // partial sums arrive as uint32 (they wrap modulo 2^32) and are read back as int32.
@@ -365,7 +412,7 @@ template <int DT, int BM, int BN, int TM, int TN>
 __device__ __forceinline__ void store_tile(const KernelArgs &args,
                                            const typename Types<DT>::acc_vec (&acc)[TM][TN],
                                            int tm, int tn, int slice, int64_t r0, int64_t c0, int lane,
-                                           int &s_last) {
+                                           int &s_last, uint32_t seen = 0u) {
     using out_t = typename Types<DT>::out_t;
     using sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type;  // int32 wraps mod 2^32
     constexpr int WAVES = (BM / (32 * TM)) * (BN / (32 * TN));
@@ -385,7 +432,9 @@ __device__ __forceinline__ void store_tile(const KernelArgs &args,
         return;
     }
     if constexpr (DT == DT_I8) {
-        if (args.reduce_in_kernel == REDUCE_ATOMIC) {
+        if (args.reduce_in_kernel == REDUCE_ATOMIC || args.reduce_in_kernel == REDUCE_ATOMIC_FLAG) {
+            if (args.reduce_in_kernel == REDUCE_ATOMIC_FLAG && slice != 0)
+                flag_take_credit(args, tm * args.tiles_n + tn, seen);
             // Relaxed device-scope adds, no return value: the kernel's end orders them
             // before anything that reads C.
             uint32_t *const cc = static_cast<uint32_t *>(args.C);

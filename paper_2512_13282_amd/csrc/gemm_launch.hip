@@ -195,8 +195,14 @@ int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr
                            args.M, args.N, args.ldc);
         if (hipGetLastError() != hipSuccess) return LAUNCH_HIP_ERROR;
     } else if (args.split_k > 1) {
-        const size_t bytes = size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
-        const int64_t tiles = args.reduce_in_kernel == REDUCE_LAST_SLICE ? int64_t(args.tiles_m) * args.tiles_n : 0;
+        const bool flag = args.reduce_in_kernel == REDUCE_ATOMIC_FLAG;
+        if (flag && (args.dtype != DT_I8 || args.epilogue != EPI_NONE ||
+                     (kConfigs[cfg].family != FAM_RING && kConfigs[cfg].family != FAM_GEMV)))
+            return LAUNCH_HIP_ERROR;
+        // REDUCE_ATOMIC_FLAG needs the counters only.
+        const size_t bytes = flag ? 0 : size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
+        const int64_t tiles = (args.reduce_in_kernel == REDUCE_LAST_SLICE || flag)
+                                  ? int64_t(args.tiles_m) * args.tiles_n : 0;
         if (static_scratch) {
             if (bytes > size_t(kStaticScratchBytes - kScratchCounterBytes) || tiles * 4 > kScratchCounterBytes)
                 return LAUNCH_SCRATCH_LIMIT;

@@ -275,6 +275,17 @@ void gemm_ring_kernel(KernelArgs args) {
         phase(I1{}, NEXT{}, I0{}, I0{}, kt + NB, j_c, I0{}, LBC{});
     };
 
+    // REDUCE_ATOMIC_FLAG: slice 0 zeroes its tile of C before loading anything; every
+    // other slice reads the tile's credit counter (every wave, so that the test stays
+    // uniform) at the first ring turn that starts at least kFlagLeadSlots slots before
+    // its end.
+    constexpr int kFlagLeadSlots = 8;
+    const bool flag = DT == DT_I8 && args.split_k > 1 && args.reduce_in_kernel == REDUCE_ATOMIC_FLAG;
+    const int flag_tile = tm * args.tiles_n + tn;
+    if (flag && slice == 0) flag_zero_tile<BM, BN, 64 * WAVES>(args, m0, n0, flag_tile);
+    const int poll_kt = (flag && slice != 0) ? (ns > kFlagLeadSlots ? (ns - kFlagLeadSlots) / NB * NB : 0) : -1;
+    uint32_t seen = 0u;
+
     if (ns > 0) {
         // Prologue: slots 0 .. NB-2 whole and the first LB loads of slot NB-1 (phase A
         // of slot 0 issues the rest, as every phase A does), then slot 0 is waited for.
@@ -283,6 +294,7 @@ void gemm_ring_kernel(KernelArgs args) {
         ring_barrier<(NB - 2) * LPS + LB>();
         load_frags(I0{}, I0{}, I0{});
         for (int kt = 0; kt < ns; kt += NB) {
+            if (kt == poll_kt) seen = load_coherent(&args.counters[flag_tile]);
             static_for<0, NB>([&](auto u) {
                 if (kt + decltype(u)::value < ns) slot(kt + decltype(u)::value, u);
             });
@@ -293,7 +305,7 @@ void gemm_ring_kernel(KernelArgs args) {
     // The ring is drained and every wave is past its last fragment read when
     // store_tile first synchronises, so it lends the last-slice flag a word.
     store_tile<DT, BM, BN, TM, TN>(args, acc, tm, tn, slice, m0 + wrow0, n0 + wcol0, lane,
-                                   *reinterpret_cast<int *>(ring_lds[0]));
+                                   *reinterpret_cast<int *>(ring_lds[0]), seen);
 }
 
 }  // namespace gemm

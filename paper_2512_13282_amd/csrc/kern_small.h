@@ -202,11 +202,13 @@ using gemv_sum_t = typename std::conditional<DT == DT_I8, uint32_t, float>::type
 // Writes `cols` results v[c] of columns n0 + c (one output row) for K slice
 // `slice`: straight into C without split-K, else into the slice's partial plane;
 // with the in-kernel reduction the workgroup arriving last for this column block
-// sums the planes in slice order; with the atomic one (int8, int32 output) every
-// slice adds into C, zeroed beforehand.  Thread t handles c = t, t + 256, ...
+// sums the planes in slice order; with the atomic ones (int8, int32 output) every
+// slice adds into C, zeroed beforehand (REDUCE_ATOMIC) or by slice 0, whose credit a
+// later slice takes first (REDUCE_ATOMIC_FLAG; `seen` is thread 0's earlier read of
+// the tile's counter).  Thread t handles c = t, t + 256, ...
 template <int DT, int COLS>
 __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_acc_t<DT> *v, int64_t n0,
-                                           int tile, int slice) {
+                                           int tile, int slice, uint32_t seen) {
     using sum_t = gemv_sum_t<DT>;
     const int64_t N = args.N;
     sum_t *ws = static_cast<sum_t *>(args.workspace);
@@ -217,7 +219,8 @@ __device__ __forceinline__ void gemv_store(const KernelArgs &args, const gemv_ac
         return;
     }
     if constexpr (DT == DT_I8) {
-        if (args.reduce_in_kernel == REDUCE_ATOMIC) {     // into C, zeroed beforehand
+        if (args.reduce_in_kernel == REDUCE_ATOMIC || args.reduce_in_kernel == REDUCE_ATOMIC_FLAG) {
+            if (args.reduce_in_kernel == REDUCE_ATOMIC_FLAG && slice != 0) flag_take_credit(args, tile, seen);
             for (int c = t; c < COLS; c += 256)
                 if (n0 + c < N)
                     __hip_atomic_fetch_add(&static_cast<uint32_t *>(args.C)[n0 + c], uint32_t(v[c]), __ATOMIC_RELAXED,
@@ -296,6 +299,13 @@ __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
     const int64_t k_begin = int64_t(slice) * args.k_chunk;
     int64_t k_end = k_begin + args.k_chunk;
     if (k_end > args.K) k_end = args.K;
+    // REDUCE_ATOMIC_FLAG: slice 0 zeroes its 1024 outputs first; the other slices read
+    // the credit counter once halfway through their rows.
+    const bool flag = DT == DT_I8 && args.split_k > 1 && args.reduce_in_kernel == REDUCE_ATOMIC_FLAG;
+    if (flag && slice == 0) flag_zero_tile<1, CB, 256>(args, 0, n0, tn);
+    bool poll_pending = flag && slice != 0;
+    const int64_t k_poll = k_begin + (k_end - k_begin) / 2;
+    uint32_t seen = 0u;
     // N * E is a multiple of 16 bytes, so a 16-byte piece is either wholly inside a row or past its end.
     bool piece_ok[PIECES];
 #pragma unroll
@@ -373,12 +383,17 @@ __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
     int64_t k0 = k_begin + wave;
     if (k0 < k_end) load_batch(b0, k0);
     for (; k0 < k_end; k0 += 2 * STEP) {
+        if (poll_pending && k0 >= k_poll) {
+            seen = load_coherent(&args.counters[tn]);
+            poll_pending = false;
+        }
         if (k0 + STEP < k_end) load_batch(b1, k0 + STEP);
         use_batch(b0);
         if (k0 + STEP >= k_end) break;
         if (k0 + 2 * STEP < k_end) load_batch(b0, k0 + 2 * STEP);
         use_batch(b1);
     }
+    if (poll_pending) seen = load_coherent(&args.counters[tn]);
 
     // The four waves' partial sums of the same columns, added in wave order.
     __shared__ acc_t red[4][CB];
@@ -395,7 +410,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
 #pragma unroll
     for (int i = 0; i < CB / 256; ++i) red[0][int(threadIdx.x) + 256 * i] = tot[i];
     __syncthreads();
-    gemv_store<DT, CB>(args, red[0], n0, tn, slice);
+    gemv_store<DT, CB>(args, red[0], n0, tn, slice, seen);
 }
 
 template <int DT>
@@ -428,11 +443,17 @@ __global__ __launch_bounds__(256) void gemv_bt_kernel(KernelArgs args) {
         brow[r] = Bb + (row_ok[r] ? n : 0) * ldb_b;
     }
 
+    // REDUCE_ATOMIC_FLAG: slice 0 zeroes its 16 outputs first; the other slices read the
+    // credit counter halfway through their K range.
+    const bool flag = DT == DT_I8 && args.split_k > 1 && args.reduce_in_kernel == REDUCE_ATOMIC_FLAG;
+    if (flag && slice == 0) flag_zero_tile<1, CB, 256>(args, 0, n0, tn);
+    uint32_t seen = 0u;
+
     acc_t acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = acc_t(0);
     // K * E is a multiple of 16 bytes and so are the slice bounds: a piece is wholly in or out.
-    for (int64_t k = k_begin + int64_t(lane) * VECE; k < k_end; k += 64 * VECE) {
+    auto step = [&](int64_t k) {
         const u32x4_t a = *reinterpret_cast<const u32x4_t *>(Ab + k * E);
         u32x4_t b[R];
 #pragma unroll
@@ -450,7 +471,14 @@ __global__ __launch_bounds__(256) void gemv_bt_kernel(KernelArgs args) {
                     acc[r] = fmaf(__uint_as_float(a[w] & 0xffff0000u), __uint_as_float(b[r][w] & 0xffff0000u), acc[r]);
                 }
             }
-    }
+    };
+    // The first half of the whole 64-piece rounds needs no bound check (every lane's piece
+    // of them lies below k_end); the counter read goes between the halves.
+    const int half = int((k_end - k_begin) / (64 * VECE) / 2);
+    int64_t k = k_begin + int64_t(lane) * VECE;
+    for (int it = 0; it < half; ++it, k += 64 * VECE) step(k);
+    if (flag && slice != 0) seen = load_coherent(&args.counters[tn]);
+    for (; k < k_end; k += 64 * VECE) step(k);
     // Butterfly over the 64 lanes: every lane ends with the wave's sums.
 #pragma unroll
     for (int r = 0; r < R; ++r)
@@ -464,7 +492,7 @@ __global__ __launch_bounds__(256) void gemv_bt_kernel(KernelArgs args) {
         res[wave * R + lane] = v;
     }
     __syncthreads();
-    gemv_store<DT, CB>(args, res, n0, tn, slice);
+    gemv_store<DT, CB>(args, res, n0, tn, slice, seen);
 }
 
 // Sums split-K partials [split][M][N] into C in slice order 0, 1, ... (the

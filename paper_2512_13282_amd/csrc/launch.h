@@ -36,8 +36,12 @@ enum { EPI_NONE = 0, EPI_I8 = 1, EPI_I16 = 2, EPI_BF16 = 3 };
 // finishes last sums the tile's partials.  REDUCE_ATOMIC (int8 with int32 output
 // only): C is zeroed first and every slice adds its partial tile into C with device
 // atomics; int32 addition modulo 2^32 is exact and order-free, so the result is the
-// same bits as the other two give, and no workspace is needed.
-enum { REDUCE_SEPARATE = 0, REDUCE_LAST_SLICE = 1, REDUCE_ATOMIC = 2 };
+// same bits as the other two give, and no workspace is needed.  REDUCE_ATOMIC_FLAG
+// (the same outputs; RING and GEMV kernels): as REDUCE_ATOMIC, but slice 0 of each
+// tile zeroes the tile inside the GEMM and hands the other slices a credit on the
+// tile's counter, so no fill kernel runs ahead of the GEMM (counters only, no
+// partial planes).
+enum { REDUCE_SEPARATE = 0, REDUCE_LAST_SLICE = 1, REDUCE_ATOMIC = 2, REDUCE_ATOMIC_FLAG = 3 };
 
 enum { LAUNCH_OK = 0, LAUNCH_HIP_ERROR = 1, LAUNCH_NO_MEMORY = 2, LAUNCH_SCRATCH_LIMIT = 3 };
 

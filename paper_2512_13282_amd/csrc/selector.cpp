@@ -76,7 +76,11 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
     // partial planes.  Atomic (int8 only): a fill launch ahead of the GEMM, the partial
     // tiles added into C, no workspace; the model's choice for int8, where it costs the
     // separate reduction's one extra launch without its partial planes (measured on the
-    // skinny shapes: it matches or beats both others).
+    // skinny shapes: it matches or beats both others).  Atomic with C zeroed by each
+    // tile's first slice (ring kernels): no fill launch; the int8 choice for ring
+    // kernels, 2-10 % faster than the fill on the skinny shapes.  The GEMV has it too,
+    // but there dozens of slices per tile take their credit from one counter word, and
+    // those same-address atomics queue (measured 60 % slower than the fill).
     double red_us = 0.0;
     pl.reduce_in_kernel = REDUCE_SEPARATE;
     if (pl.split_k > 1) {
@@ -85,13 +89,17 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
         const double in_kernel_us = trips * chip.round_trip_us;
         const double separate_us = chip.launch_us;
         int32_t mode = reduce >= 0 ? reduce
-                     : p.dtype == DT_I8 ? REDUCE_ATOMIC
+                     : p.dtype == DT_I8 ? (c.family == FAM_RING ? REDUCE_ATOMIC_FLAG : REDUCE_ATOMIC)
                      : (in_kernel_us <= separate_us ? REDUCE_LAST_SLICE : REDUCE_SEPARATE);
-        if (mode == REDUCE_ATOMIC && p.dtype != DT_I8) mode = REDUCE_SEPARATE;
+        if ((mode == REDUCE_ATOMIC || mode == REDUCE_ATOMIC_FLAG) && p.dtype != DT_I8) mode = REDUCE_SEPARATE;
+        if (mode == REDUCE_ATOMIC_FLAG && c.family != FAM_RING && c.family != FAM_GEMV) mode = REDUCE_ATOMIC;
         pl.reduce_in_kernel = mode;
-        red_us = mode == REDUCE_LAST_SLICE ? in_kernel_us : separate_us;   // atomic: the fill launch
+        // atomic: the fill launch; atomic with slice 0's zeros: their round trip
+        red_us = mode == REDUCE_LAST_SLICE ? in_kernel_us
+               : mode == REDUCE_ATOMIC_FLAG ? chip.round_trip_us : separate_us;
     }
-    const bool partial_planes = pl.split_k > 1 && pl.reduce_in_kernel != REDUCE_ATOMIC;
+    const bool partial_planes =
+        pl.split_k > 1 && pl.reduce_in_kernel != REDUCE_ATOMIC && pl.reduce_in_kernel != REDUCE_ATOMIC_FLAG;
     pl.workspace_bytes = partial_planes ? int64_t(pl.split_k) * p.M * p.N * 4 : 0;
 
     // Compute: whole rounds of resident workgroups (wave quantization).

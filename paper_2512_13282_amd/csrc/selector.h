@@ -18,8 +18,8 @@ struct Problem {
 struct Plan {
     int32_t config;      // index into kConfigs
     int32_t split_k;     // >= 1
-    int32_t reduce_in_kernel;  // split-K reduction: REDUCE_SEPARATE, REDUCE_LAST_SLICE or
-                               // REDUCE_ATOMIC (launch.h)
+    int32_t reduce_in_kernel;  // split-K reduction: REDUCE_SEPARATE, REDUCE_LAST_SLICE,
+                               // REDUCE_ATOMIC or REDUCE_ATOMIC_FLAG (launch.h)
     int64_t k_chunk;     // K elements per slice (multiple of the stage depth)
     int64_t tiles_m, tiles_n;
     int64_t grid;

@@ -144,7 +144,7 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
     try:
         for cfg in range(n_cfg):
             for split in (SPLITS_SMALL_M if M < 256 else SPLITS_LARGE):
-                reductions = (0, 1, 2) if dtype == "int8" else (0, 1)   # atomic: int8 only
+                reductions = (0, 1, 2, 3) if dtype == "int8" else (0, 1)   # atomic: int8 only
                 for reduce in ((-1,) if split == 1 else reductions):
                     if b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, cfg, split) != 0:
                         continue
@@ -200,7 +200,7 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
 def write_inc(entries, path=OUT):
     lines = ["// Generated by `python -m paper_2512_13282_amd.tune` from on-device measurements",
              "// (fastest plan per shape over sustained runs of back-to-back launches).  Fields: dtype, M, N, K, config, split_k, reduce,",
-             "// (split-K reduction: 0 separate kernel, 1 in-kernel by the last slice, 2 atomic adds into C, -1 the model's choice), B layout",
+             "// (split-K reduction: 0 separate kernel, 1 in-kernel by the last slice, 2 atomic adds into C zeroed by a fill kernel, 3 atomic adds into C zeroed by the first slice, -1 the model's choice), B layout",
              "// (1: column-major).",
              "// Consulted by select_plan before the analytical model for an exact shape match."]
     for e in entries:

@@ -83,9 +83,10 @@ def test_force_plan_validation():
 
 def test_force_reduce_validation():
     assert b.gemm_force_reduce(7, 0) == b.GEMM_ERR_INVALID_VALUE
-    assert b.gemm_force_reduce(I8, 3) == b.GEMM_ERR_INVALID_VALUE
+    assert b.gemm_force_reduce(I8, 4) == b.GEMM_ERR_INVALID_VALUE
     assert b.gemm_force_reduce(I8, -2) == b.GEMM_ERR_INVALID_VALUE
-    for mode in (b.GEMM_REDUCE_SEPARATE, b.GEMM_REDUCE_LAST_SLICE, b.GEMM_REDUCE_ATOMIC, -1):
+    for mode in (b.GEMM_REDUCE_SEPARATE, b.GEMM_REDUCE_LAST_SLICE, b.GEMM_REDUCE_ATOMIC,
+                 b.GEMM_REDUCE_ATOMIC_FLAG, -1):
         assert b.gemm_force_reduce(I8, mode) == b.GEMM_OK
 
 

@@ -89,7 +89,8 @@ def check_bf16(A, B, C, bt=False):
     assert np.all(np.abs(got - exact) <= bound)
 
 
-@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1), (3, 2)], ids=["s1", "s3sep", "s3fused", "s3atomic"])
+@pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1), (3, 2), (3, 3)],
+                         ids=["s1", "s3sep", "s3fused", "s3atomic", "s3flag"])
 @pytest.mark.parametrize("config", CONFIGS)
 def test_reduced_outputs_every_family(config, split, reduce):
     for i, (M, N, K) in enumerate(SHAPES):

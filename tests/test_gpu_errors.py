@@ -1,7 +1,8 @@
 """Error paths of the C ABI that need a GPU: a split-K workspace that cannot be allocated
 returns GEMM_ERR_NO_MEMORY with nothing queued and C untouched, and the next call, with
-allocation possible again, runs normally; the atomic reduction, which needs no workspace,
-is unaffected (needs an MI355X)."""
+allocation possible again, runs normally (also for the atomic reduction whose C is zeroed
+by the first slice: it needs per-tile counters); the atomic reduction with a fill kernel,
+which needs no workspace, is unaffected (needs an MI355X)."""
 import numpy as np
 import pytest
 import torch
@@ -35,7 +36,8 @@ def _call(fn, A, B, sentinel):
     return rc, dC.cpu().numpy()[: M * ldc].reshape(M, ldc)[:, :N]
 
 
-@pytest.mark.parametrize("config,split,reduce", [(30, 8, 0), (28, 4, 1)], ids=["separate-reduce", "in-kernel"])
+@pytest.mark.parametrize("config,split,reduce", [(30, 8, 0), (28, 4, 1), (28, 4, 3)],
+                         ids=["separate-reduce", "in-kernel", "atomic-flag-counters"])
 def test_workspace_failure_then_recovery(monkeypatch, config, split, reduce):
     M, K, N = 64, 4096, 2048
     A, B = inputs.make_inputs("int8", M, N, K, seed=9)

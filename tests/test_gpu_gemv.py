@@ -39,10 +39,11 @@ def _check_bt(dtype, A, Bt, C):
 # N ragged against the 1024-column (row-major) and 16-column (column-major) blocks;
 # K from one 16-byte piece to several slices.
 SHAPES = [(16, 16), (48, 272), (1040, 1040), (2064, 4096), (4112, 528), (14336, 4096), (4096, 14336)]
-SPLITS = [(1, -1), (3, 0), (3, 1), (7, 1), (5, 2)]
+SPLITS = [(1, -1), (3, 0), (3, 1), (7, 1), (5, 2), (5, 3), (32, 3)]
+SPLIT_IDS = ["s1", "s3sep", "s3fused", "s7fused", "s5atomic", "s5flag", "s32flag"]
 
 
-@pytest.mark.parametrize("split,reduce", SPLITS, ids=["s1", "s3sep", "s3fused", "s7fused", "s5atomic"])
+@pytest.mark.parametrize("split,reduce", SPLITS, ids=SPLIT_IDS)
 @pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
 def test_gemv_row_major_b(dtype, split, reduce):
     g.force(dtype, b.GEMM_KERNEL_AUTO, GEMV_RM, split, reduce)
@@ -52,7 +53,7 @@ def test_gemv_row_major_b(dtype, split, reduce):
         (g.check_i8 if dtype == I8 else g.check_bf16)(A, B, g.gemm_gpu(dtype, A, B))
 
 
-@pytest.mark.parametrize("split,reduce", SPLITS, ids=["s1", "s3sep", "s3fused", "s7fused", "s5atomic"])
+@pytest.mark.parametrize("split,reduce", SPLITS, ids=SPLIT_IDS)
 @pytest.mark.parametrize("dtype", [I8, BF], ids=["i8", "bf16"])
 def test_gemv_column_major_b(dtype, split, reduce):
     g.force(dtype, b.GEMM_KERNEL_AUTO, GEMV_BT, split, reduce)

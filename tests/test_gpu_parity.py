@@ -23,6 +23,7 @@ NUM_CONFIGS = 41
 GENERIC_CONFIGS = (0, 1)
 GEMV_CONFIGS = (26, 27)      # M = 1 only: tests/test_gpu_gemv.py
 TILE_CONFIGS = [c for c in range(NUM_CONFIGS) if c not in GEMV_CONFIGS]
+RING_CONFIGS = [c for c in range(16, NUM_CONFIGS) if c not in GEMV_CONFIGS]
 
 
 @pytest.fixture(autouse=True)
@@ -200,8 +201,8 @@ def test_int8_split_k_is_invariant():
     A, B = _inputs(I8, M, N, K, seed=9)
     outs = []
     for split in (1, 2, 5, 16, 32):
-        for reduce in (-1, b.GEMM_REDUCE_ATOMIC):
-            g.force(I8, b.GEMM_KERNEL_AUTO, 3, split, reduce)
+        for config, reduce in ((3, -1), (3, b.GEMM_REDUCE_ATOMIC), (28, b.GEMM_REDUCE_ATOMIC_FLAG)):
+            g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
             outs.append(g.gemm_gpu(I8, A, B))
     for o in outs[1:]:
         assert np.array_equal(o, outs[0])
@@ -237,8 +238,10 @@ def test_split_k_workspace_reuse_across_shapes_and_streams():
         ref, _ = oracle.get().gemm_i8_i32(A, B)
         cases.append((M, N, K, A, B, ref))
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
-    for reduce in (1, 0, 2):
-        for config, split in ((3, 6), (6, 16), (14, 5), (10, 3)):
+    tile_plans = ((3, 6), (6, 16), (14, 5), (10, 3))
+    ring_plans = ((28, 6), (31, 16), (20, 5), (38, 3))
+    for reduce, plans in ((1, tile_plans), (0, tile_plans), (2, tile_plans), (3, ring_plans), (1, ring_plans)):
+        for config, split in plans:
             g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
             print(f"workspace reuse config={config} split={split} reduce={reduce}", flush=True)
             outs = []
@@ -290,6 +293,37 @@ def test_int8_atomic_reduction(config, split, bt):
             assert (host[M * ldc:] == sentinel).all(), "memory past C was written"
 
 
+@pytest.mark.parametrize("config", RING_CONFIGS)
+def test_int8_atomic_flag_every_ring_config(config):
+    """Atomic split-K reduction with C zeroed inside the GEMM by each tile's first K slice,
+    whose signal the other slices wait for before adding.  Exact against the oracle on
+    ragged shapes and split factors, with slices longer and shorter than the lead at which
+    the signal is read; the row padding and the memory past C untouched; a second call into
+    the same (now non-zero) C gives the same result."""
+    for split in (2, 3, 9):
+        g.force(I8, b.GEMM_KERNEL_AUTO, config, split, b.GEMM_REDUCE_ATOMIC_FLAG)
+        for M, N, K in [(75, 272, 2304), (1, 4112, 1024), (33, 48, 4096), (300, 528, 640)]:
+            A, B = _inputs(I8, M, N, K, seed=70 + M + split)
+            p = b.gemm_plan(I8, M, N, K, K, N, N + 5, 1 << 40, 2 << 40, 3 << 40)
+            assert p["split_k"] > 1 and p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG, p
+            assert p["workspace_bytes"] == 0, p
+            dA, lda = g.to_dev(A)
+            dB, ldb = g.to_dev(B)
+            sentinel = -515151
+            dC, ldc = g.out_buffer(M, N, I8, pad_cols=5, sentinel=sentinel)
+            ref, ovf = oracle.get().gemm_i8_i32(A, B)
+            assert ovf == 0
+            for rep in range(2):
+                print(f"atomic flag config={config} split={split} shape={(M, N, K)} rep={rep}", flush=True)
+                assert g.call(I8, M, N, K, dA, lda, dB, ldb, dC, ldc) == b.GEMM_OK
+                torch.cuda.synchronize()
+                host = dC.cpu().numpy()
+                C = host[: M * ldc].reshape(M, ldc)
+                assert np.array_equal(C[:, :N], ref), np.argwhere(C[:, :N] != ref)[:3].tolist()
+                assert (C[:, N:] == sentinel).all(), "row padding of C was written"
+                assert (host[M * ldc:] == sentinel).all(), "memory past C was written"
+
+
 def test_release_workspace_then_reuse():
     M, N, K = 48, 512, 4096
     A, B = _inputs(I8, M, N, K, seed=50)
@@ -325,8 +359,9 @@ def test_int8_extremes_largest_k(config):
     assert (C[:, ::2] == -16256 * K).all() and (C[:, 1::2] == 234881024).all()
 
 
-SPLIT_REDUCTIONS = [(1, -1), (4, b.GEMM_REDUCE_SEPARATE), (4, b.GEMM_REDUCE_LAST_SLICE), (4, b.GEMM_REDUCE_ATOMIC),
-                    (2, b.GEMM_REDUCE_ATOMIC)]
+SPLIT_REDUCTIONS = [(3, 1, -1), (3, 4, b.GEMM_REDUCE_SEPARATE), (3, 4, b.GEMM_REDUCE_LAST_SLICE),
+                    (3, 4, b.GEMM_REDUCE_ATOMIC), (3, 2, b.GEMM_REDUCE_ATOMIC), (28, 4, b.GEMM_REDUCE_ATOMIC_FLAG),
+                    (28, 2, b.GEMM_REDUCE_ATOMIC_FLAG)]   # (config, split, reduction)
 
 
 def test_int8_wraps_past_int32():
@@ -337,10 +372,10 @@ def test_int8_wraps_past_int32():
     B = np.full((K, N), -128, np.int8)
     ref, ovf = oracle.get().gemm_i8_i32(A[:1], B[:, :1])
     assert ovf == 1
-    for split, reduce in SPLIT_REDUCTIONS:
-        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split, reduce)
+    for config, split, reduce in SPLIT_REDUCTIONS:
+        g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
         C = g.gemm_gpu(I8, A, B)
-        assert (C == ref[0, 0]).all(), (split, reduce, np.unique(C)[:4])
+        assert (C == ref[0, 0]).all(), (config, split, reduce, np.unique(C)[:4])
 
 
 def test_int8_partials_wrap_total_fits():
@@ -354,10 +389,10 @@ def test_int8_partials_wrap_total_fits():
     B = np.full((K, N), -128, np.int8)
     ref, ovf = oracle.get().gemm_i8_i32(A[:1], B[:, :1])
     assert ovf == 0 and int(ref[0, 0]) == 2 ** 24
-    for split, reduce in SPLIT_REDUCTIONS:
-        g.force(I8, b.GEMM_KERNEL_AUTO, 3, split, reduce)
+    for config, split, reduce in SPLIT_REDUCTIONS:
+        g.force(I8, b.GEMM_KERNEL_AUTO, config, split, reduce)
         C = g.gemm_gpu(I8, A, B)
-        assert (C == 2 ** 24).all(), (split, reduce, np.unique(C)[:4])
+        assert (C == 2 ** 24).all(), (config, split, reduce, np.unique(C)[:4])
 
 
 def test_torch_helpers():

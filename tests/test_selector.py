@@ -30,10 +30,13 @@ def check_invariants(p, dtype, M, N, K):
         assert p["split_k"] * p["k_chunk"] >= K > (p["split_k"] - 1) * p["k_chunk"]
     else:
         assert p["split_k"] == 1
-    planes = p["split_k"] > 1 and p["reduce_in_kernel"] != b.GEMM_REDUCE_ATOMIC
+    atomic = p["reduce_in_kernel"] in (b.GEMM_REDUCE_ATOMIC, b.GEMM_REDUCE_ATOMIC_FLAG)
+    planes = p["split_k"] > 1 and not atomic
     assert p["workspace_bytes"] == (p["split_k"] * M * N * 4 if planes else 0)
-    if p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC:
+    if atomic:
         assert dtype == I8 and p["split_k"] > 1
+    if p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG:
+        assert p["kernel"] in (b.GEMM_KERNEL_RING, b.GEMM_KERNEL_GEMV)
     assert p["grid"] < 2 ** 31
 
 
@@ -157,8 +160,9 @@ def test_tuned_plans_skip_misaligned_operands():
 
 def test_split_k_reduction_choice():
     """bf16: a small per-tile reduction (one row of output) is summed in the GEMM kernel by the
-    last slice, a large one (many rows times many slices) by the separate kernel.  int8: the
-    atomic reduction, whatever the size.  Forcing a reduction is reflected in the plan, and
+    last slice, a large one (many rows times many slices) by the separate kernel.  int8: an
+    atomic reduction, whatever the size: C zeroed by each tile's first slice on ring kernels,
+    by a fill kernel on the others.  Forcing a reduction is reflected in the plan, and
     split_k == 1 reports none."""
     try:
         for d in (I8, BF):
@@ -176,6 +180,11 @@ def test_split_k_reduction_choice():
             assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == mode
         assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 3, 1) == b.GEMM_OK
         assert plan(I8, 128, 4096, 16384)["reduce_in_kernel"] == 0
+        b.gemm_force_reduce(I8, -1)
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 28, 4) == b.GEMM_OK      # ring_32x256_w4_r4
+        assert plan(I8, 16, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_GEMV, 26, 8) == b.GEMM_OK      # gemv_1024
+        assert plan(I8, 1, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC
     finally:
         for d in (I8, BF):
             b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
@@ -183,8 +192,9 @@ def test_split_k_reduction_choice():
 
 
 def test_atomic_reduction_plans():
-    """The atomic split-K reduction is int8-only and needs no workspace; asked of bf16, the
-    plan takes the separate reduction instead."""
+    """The atomic split-K reductions are int8-only and need no partial planes; asked of bf16,
+    the plan takes the separate reduction instead.  The one whose C is zeroed by the first
+    slice runs on ring and GEMV kernels; another family asked for it keeps the fill kernel."""
     try:
         for d in (I8, BF):
             assert b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, 28, 4) == b.GEMM_OK
@@ -196,6 +206,21 @@ def test_atomic_reduction_plans():
         check_invariants(q, BF, 16, 14336, 4096)
         assert q["split_k"] == 4 and q["reduce_in_kernel"] == b.GEMM_REDUCE_SEPARATE
         assert q["workspace_bytes"] == 4 * 16 * 14336 * 4
+        # C zeroed by the first slice: ring and GEMV kernels only, others keep the fill kernel
+        for d in (I8, BF):
+            assert b.gemm_force_reduce(d, b.GEMM_REDUCE_ATOMIC_FLAG) == b.GEMM_OK
+        p = plan(I8, 16, 14336, 4096)
+        check_invariants(p, I8, 16, 14336, 4096)
+        assert p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG and p["workspace_bytes"] == 0
+        assert plan(BF, 16, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_SEPARATE
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 14, 4) == b.GEMM_OK      # stream_32x256_s4
+        p = plan(I8, 16, 14336, 4096)
+        check_invariants(p, I8, 16, 14336, 4096)
+        assert p["kernel"] == b.GEMM_KERNEL_SKINNY and p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_GEMV, 26, 8) == b.GEMM_OK      # gemv_1024
+        p = plan(I8, 1, 14336, 4096)
+        check_invariants(p, I8, 1, 14336, 4096)
+        assert p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG
     finally:
         for d in (I8, BF):
             b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
