@@ -162,7 +162,8 @@ __device__ __forceinline__ T load_coherent(const T *p) {
 constexpr unsigned kCreditPollLimit = 1u << 20;
 
 // Slice 0's part, by all NT threads of the workgroup: the BM x BN tile at (m0, n0),
-// clipped to M x N.
+// clipped to M x N.  `tile` numbers the tile; its counter is word
+// tile * kFlagCounterStride.
 template <int BM, int BN, int NT>
 __device__ __forceinline__ void flag_zero_tile(const KernelArgs &args, int64_t m0, int64_t n0, int tile) {
     uint32_t *const cc = static_cast<uint32_t *>(args.C);
@@ -175,7 +176,7 @@ __device__ __forceinline__ void flag_zero_tile(const KernelArgs &args, int64_t m
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's zeros are complete
     __syncthreads();                                   // ... and every thread's
     if (threadIdx.x == 0)
-        __hip_atomic_fetch_add(&args.counters[tile], uint32_t(args.split_k - 1), __ATOMIC_RELAXED,
+        __hip_atomic_fetch_add(&args.counters[tile * kFlagCounterStride], uint32_t(args.split_k - 1), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -186,10 +187,11 @@ __device__ __forceinline__ void flag_take_credit(const KernelArgs &args, int til
         uint32_t v = seen;
         for (unsigned i = 0; v == 0u && i < kCreditPollLimit; ++i) {
             __builtin_amdgcn_s_sleep(8);
-            v = load_coherent(&args.counters[tile]);
+            v = load_coherent(&args.counters[tile * kFlagCounterStride]);
         }
         if (v != 0u)
-            __hip_atomic_fetch_sub(&args.counters[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_sub(&args.counters[tile * kFlagCounterStride], 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
 }

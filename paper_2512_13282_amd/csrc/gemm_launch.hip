@@ -74,13 +74,13 @@ static bool fail_workspace_for_test() {
     return e != nullptr && e[0] == '1';
 }
 
-static int acquire_workspace(hipStream_t stream, size_t partial_bytes, int64_t tiles, void **partials,
+static int acquire_workspace(hipStream_t stream, size_t partial_bytes, int64_t counter_words, void **partials,
                              uint32_t **counters) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return LAUNCH_HIP_ERROR;
     std::lock_guard<std::mutex> lk(g_ws_mu);
     Workspace &w = g_ws[{dev, reinterpret_cast<uintptr_t>(stream)}];
-    if ((w.partial_bytes < partial_bytes || w.counter_cap < tiles) && fail_workspace_for_test())
+    if ((w.partial_bytes < partial_bytes || w.counter_cap < counter_words) && fail_workspace_for_test())
         return LAUNCH_NO_MEMORY;
     if (w.partial_bytes < partial_bytes) {
         if (w.partials != nullptr && hipFreeAsync(w.partials, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
@@ -94,10 +94,10 @@ static int acquire_workspace(hipStream_t stream, size_t partial_bytes, int64_t t
         }
         w.partial_bytes = bytes;
     }
-    if (w.counter_cap < tiles) {
+    if (w.counter_cap < counter_words) {
         if (w.counters != nullptr && hipFreeAsync(w.counters, stream) != hipSuccess) return LAUNCH_HIP_ERROR;
         w.counters = nullptr;
-        const int64_t cap = int64_t(grow(size_t(tiles), size_t(w.counter_cap), 4096));
+        const int64_t cap = int64_t(grow(size_t(counter_words), size_t(w.counter_cap), 4096));
         w.counter_cap = 0;
         void *p = nullptr;
         if (hipMallocAsync(&p, size_t(cap) * 4, stream) != hipSuccess || p == nullptr) {
@@ -199,12 +199,12 @@ int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr
         if (flag && (args.dtype != DT_I8 || args.epilogue != EPI_NONE ||
                      (kConfigs[cfg].family != FAM_RING && kConfigs[cfg].family != FAM_GEMV)))
             return LAUNCH_HIP_ERROR;
-        // REDUCE_ATOMIC_FLAG needs the counters only.
+        // REDUCE_ATOMIC_FLAG needs the counters only, one 128-byte line per tile.
         const size_t bytes = flag ? 0 : size_t(args.split_k) * size_t(args.M) * size_t(args.N) * 4;
-        const int64_t tiles = (args.reduce_in_kernel == REDUCE_LAST_SLICE || flag)
-                                  ? int64_t(args.tiles_m) * args.tiles_n : 0;
+        const int64_t counter_words = args.reduce_in_kernel == REDUCE_LAST_SLICE ? int64_t(args.tiles_m) * args.tiles_n
+                              : flag ? int64_t(args.tiles_m) * args.tiles_n * kFlagCounterStride : 0;
         if (static_scratch) {
-            if (bytes > size_t(kStaticScratchBytes - kScratchCounterBytes) || tiles * 4 > kScratchCounterBytes)
+            if (bytes > size_t(kStaticScratchBytes - kScratchCounterBytes) || counter_words * 4 > kScratchCounterBytes)
                 return LAUNCH_SCRATCH_LIMIT;
             uint8_t *base = nullptr;
             const int rc = static_scratch_address(&base);
@@ -213,14 +213,14 @@ int launch_gemm(const KernelArgs &a, int32_t cfg, int64_t grid, void *stream_ptr
             args.workspace = base + kScratchCounterBytes;
             // The array keeps the previous call's contents: the arrival counters must start
             // at zero (a fill kernel, which a stream capture records like any launch).
-            if (tiles > 0) {
-                int64_t blocks = (tiles + 255) / 256;
+            if (counter_words > 0) {
+                int64_t blocks = (counter_words + 255) / 256;
                 hipLaunchKernelGGL(zero_u32_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, args.counters,
-                                   tiles);
+                                   counter_words);
                 if (hipGetLastError() != hipSuccess) return LAUNCH_HIP_ERROR;
             }
         } else {
-            const int rc = acquire_workspace(stream, bytes, tiles, &args.workspace, &args.counters);
+            const int rc = acquire_workspace(stream, bytes, counter_words, &args.workspace, &args.counters);
             if (rc != LAUNCH_OK) return rc;
         }
     }

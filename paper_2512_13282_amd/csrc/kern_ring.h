@@ -294,7 +294,7 @@ void gemm_ring_kernel(KernelArgs args) {
         ring_barrier<(NB - 2) * LPS + LB>();
         load_frags(I0{}, I0{}, I0{});
         for (int kt = 0; kt < ns; kt += NB) {
-            if (kt == poll_kt) seen = load_coherent(&args.counters[flag_tile]);
+            if (kt == poll_kt) seen = load_coherent(&args.counters[flag_tile * kFlagCounterStride]);
             static_for<0, NB>([&](auto u) {
                 if (kt + decltype(u)::value < ns) slot(kt + decltype(u)::value, u);
             });
