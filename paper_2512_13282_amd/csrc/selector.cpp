@@ -77,10 +77,8 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
     // tiles added into C, no workspace; the model's choice for int8, where it costs the
     // separate reduction's one extra launch without its partial planes (measured on the
     // skinny shapes: it matches or beats both others).  Atomic with C zeroed by each
-    // tile's first slice (ring kernels): no fill launch; the int8 choice for ring
-    // kernels, 2-10 % faster than the fill on the skinny shapes.  The GEMV has it too,
-    // but there dozens of slices per tile take their credit from one counter word, and
-    // those same-address atomics queue (measured 60 % slower than the fill).
+    // tile's first slice (ring and GEMV kernels): no fill launch; the int8 choice for
+    // those kernels, 2-12 % faster than the fill on the skinny shapes.
     double red_us = 0.0;
     pl.reduce_in_kernel = REDUCE_SEPARATE;
     if (pl.split_k > 1) {
@@ -89,7 +87,8 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
         const double in_kernel_us = trips * chip.round_trip_us;
         const double separate_us = chip.launch_us;
         int32_t mode = reduce >= 0 ? reduce
-                     : p.dtype == DT_I8 ? (c.family == FAM_RING ? REDUCE_ATOMIC_FLAG : REDUCE_ATOMIC)
+                     : p.dtype == DT_I8 ? ((c.family == FAM_RING || c.family == FAM_GEMV) ? REDUCE_ATOMIC_FLAG
+                                                                                       : REDUCE_ATOMIC)
                      : (in_kernel_us <= separate_us ? REDUCE_LAST_SLICE : REDUCE_SEPARATE);
         if ((mode == REDUCE_ATOMIC || mode == REDUCE_ATOMIC_FLAG) && p.dtype != DT_I8) mode = REDUCE_SEPARATE;
         if (mode == REDUCE_ATOMIC_FLAG && c.family != FAM_RING && c.family != FAM_GEMV) mode = REDUCE_ATOMIC;

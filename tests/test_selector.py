@@ -161,8 +161,8 @@ def test_tuned_plans_skip_misaligned_operands():
 def test_split_k_reduction_choice():
     """bf16: a small per-tile reduction (one row of output) is summed in the GEMM kernel by the
     last slice, a large one (many rows times many slices) by the separate kernel.  int8: an
-    atomic reduction, whatever the size: C zeroed by each tile's first slice on ring kernels,
-    by a fill kernel on the others.  Forcing a reduction is reflected in the plan, and
+    atomic reduction, whatever the size: C zeroed by each tile's first slice on ring and GEMV
+    kernels, by a fill kernel on the others.  Forcing a reduction is reflected in the plan, and
     split_k == 1 reports none."""
     try:
         for d in (I8, BF):
@@ -184,7 +184,9 @@ def test_split_k_reduction_choice():
         assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 28, 4) == b.GEMM_OK      # ring_32x256_w4_r4
         assert plan(I8, 16, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG
         assert b.gemm_force_plan(I8, b.GEMM_KERNEL_GEMV, 26, 8) == b.GEMM_OK      # gemv_1024
-        assert plan(I8, 1, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC
+        assert plan(I8, 1, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 14, 4) == b.GEMM_OK      # stream_32x256_s4
+        assert plan(I8, 16, 14336, 4096)["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC
     finally:
         for d in (I8, BF):
             b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
