@@ -298,8 +298,8 @@ def test_int8_atomic_flag_every_ring_config(config):
     """Atomic split-K reduction with C zeroed inside the GEMM by each tile's first K slice,
     whose signal the other slices wait for before adding.  Exact against the oracle on
     ragged shapes and split factors, with slices longer and shorter than the lead at which
-    the signal is read; the row padding and the memory past C untouched; a second call into
-    the same (now non-zero) C gives the same result."""
+    the signal is read, C's row pitch N + 5 and N; the row padding and the memory past C
+    untouched; a second call into the same (now non-zero) C gives the same result."""
     for split in (2, 3, 9):
         g.force(I8, b.GEMM_KERNEL_AUTO, config, split, b.GEMM_REDUCE_ATOMIC_FLAG)
         for M, N, K in [(75, 272, 2304), (1, 4112, 1024), (33, 48, 4096), (300, 528, 640)]:
@@ -310,11 +310,12 @@ def test_int8_atomic_flag_every_ring_config(config):
             dA, lda = g.to_dev(A)
             dB, ldb = g.to_dev(B)
             sentinel = -515151
-            dC, ldc = g.out_buffer(M, N, I8, pad_cols=5, sentinel=sentinel)
             ref, ovf = oracle.get().gemm_i8_i32(A, B)
             assert ovf == 0
-            for rep in range(2):
-                print(f"atomic flag config={config} split={split} shape={(M, N, K)} rep={rep}", flush=True)
+            for pad, rep in ((5, 0), (5, 1), (0, 0), (0, 1)):
+                if rep == 0:
+                    dC, ldc = g.out_buffer(M, N, I8, pad_cols=pad, sentinel=sentinel)
+                print(f"atomic flag config={config} split={split} shape={(M, N, K)} ldc={ldc} rep={rep}", flush=True)
                 assert g.call(I8, M, N, K, dA, lda, dB, ldb, dC, ldc) == b.GEMM_OK
                 torch.cuda.synchronize()
                 host = dC.cpu().numpy()

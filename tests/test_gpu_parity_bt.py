@@ -57,15 +57,17 @@ RING_BT_CONFIGS = [c for c in BT_CONFIGS if c >= 16]
 @pytest.mark.parametrize("config", RING_BT_CONFIGS)
 def test_int8_atomic_flag_bt(config):
     """Column-major B with the atomic split-K reduction whose C is zeroed by each tile's first
-    K slice: exact against the oracle for every ring configuration, ragged N, two splits."""
+    K slice: exact against the oracle for every ring configuration, ragged N, two splits, C's
+    row pitch unpadded and padded to a multiple of 4."""
     for split in (2, 5):
         g.force(I8, b.GEMM_KERNEL_AUTO, config, split, b.GEMM_REDUCE_ATOMIC_FLAG)
         for i, (M, N, K) in enumerate([(37, 45, 2048), (257, 529, 2064), (1, 300, 4096)]):
             p = b.gemm_plan(I8, M, N, K, K, K, N, 1 << 40, 2 << 40, 3 << 40, trans_b=True)
             assert p["split_k"] > 1 and p["reduce_in_kernel"] == b.GEMM_REDUCE_ATOMIC_FLAG, p
             A, Bt = _inputs_bt(I8, M, N, K, seed=450 + i + split)
-            print(f"bt atomic flag config={config} split={split} shape={(M, N, K)}", flush=True)
-            _check_bt(I8, A, Bt, g.gemm_gpu_bt(I8, A, Bt))
+            for pad_c in (0, (-N) % 4 + 4):
+                print(f"bt atomic flag config={config} split={split} shape={(M, N, K)} ldc={N + pad_c}", flush=True)
+                _check_bt(I8, A, Bt, g.gemm_gpu_bt(I8, A, Bt, pad=(0, 0, pad_c)))
 
 
 @pytest.mark.parametrize("split,reduce", [(1, -1), (3, 0), (3, 1), (3, 2)], ids=["s1", "s3sep", "s3fused", "s3atomic"])
