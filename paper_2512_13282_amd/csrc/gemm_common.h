@@ -121,9 +121,10 @@ __device__ __forceinline__ void map_tile(const KernelArgs &a, int &tm, int &tn, 
 // for the next launch on the stream.  Both sum in the fixed slice order
 // 0, 1, ..., so fp32 results are identical run to run whichever slice finishes
 // last and whichever reduction runs.  int8 with int32 output may instead add
-// every slice's partial tile straight into C, zeroed beforehand, with device
-// atomics (REDUCE_ATOMIC): integer addition is exact and order-free, so the bits
-// are the same, with no workspace and no second pass over partial planes.
+// every slice's partial tile straight into C with device atomics, C zeroed by a
+// fill kernel beforehand (REDUCE_ATOMIC) or by each tile's first slice inside the
+// GEMM (REDUCE_ATOMIC_FLAG, below): integer addition is exact and order-free, so
+// the bits are the same, with no partial planes and no second pass over them.
 //
 // The slices of a tile run on different XCDs, whose L2 caches are not kept
 // coherent with each other for ordinary accesses.  Instead of device-scope
