@@ -159,12 +159,17 @@ __device__ __forceinline__ T load_coherent(const T *p) {
 // slice depends only on slice 0 of its tile, which waits for nothing; on every XCD
 // the slice-0 workgroups have the lowest numbers (map_tile) and start first.  The
 // polling is bounded all the same (about a second), so a slice 0 that never runs
-// cannot hang the kernel; its tile's result is then wrong.
+// cannot hang the kernel; its tile's result is then wrong, and a credit it hands
+// out later stays on the counter for a later call on the stream to take too early
+// (a GPU on which slice-0 workgroups cannot start for that long is out of scope).
 constexpr unsigned kCreditPollLimit = 1u << 20;
 
+__device__ __forceinline__ uint32_t *flag_counter(const KernelArgs &args, int tile) {
+    return args.counters + int64_t(tile) * kFlagCounterStride;
+}
+
 // Slice 0's part, by all NT threads of the workgroup: the BM x BN tile at (m0, n0),
-// clipped to M x N.  `tile` numbers the tile; its counter is word
-// tile * kFlagCounterStride.
+// clipped to M x N.  `tile` numbers the tile (its counter: flag_counter).
 template <int BM, int BN, int NT>
 __device__ __forceinline__ void flag_zero_tile(const KernelArgs &args, int64_t m0, int64_t n0, int tile) {
     uint32_t *const cc = static_cast<uint32_t *>(args.C);
@@ -177,7 +182,7 @@ __device__ __forceinline__ void flag_zero_tile(const KernelArgs &args, int64_t m
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this thread's zeros are complete
     __syncthreads();                                   // ... and every thread's
     if (threadIdx.x == 0)
-        __hip_atomic_fetch_add(&args.counters[tile * kFlagCounterStride], uint32_t(args.split_k - 1), __ATOMIC_RELAXED,
+        __hip_atomic_fetch_add(flag_counter(args, tile), uint32_t(args.split_k - 1), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -188,11 +193,9 @@ __device__ __forceinline__ void flag_take_credit(const KernelArgs &args, int til
         uint32_t v = seen;
         for (unsigned i = 0; v == 0u && i < kCreditPollLimit; ++i) {
             __builtin_amdgcn_s_sleep(8);
-            v = load_coherent(&args.counters[tile * kFlagCounterStride]);
+            v = load_coherent(flag_counter(args, tile));
         }
-        if (v != 0u)
-            __hip_atomic_fetch_sub(&args.counters[tile * kFlagCounterStride], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+        if (v != 0u) __hip_atomic_fetch_sub(flag_counter(args, tile), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
 }

@@ -277,8 +277,8 @@ void gemm_ring_kernel(KernelArgs args) {
 
     // REDUCE_ATOMIC_FLAG: slice 0 zeroes its tile of C before loading anything; every
     // other slice reads the tile's credit counter (every wave, so that the test stays
-    // uniform) at the first ring turn that starts at least kFlagLeadSlots slots before
-    // its end.
+    // uniform) at the last ring turn that starts at least kFlagLeadSlots slots before
+    // its end (at the first turn if the slice is shorter than that).
     constexpr int kFlagLeadSlots = 8;
     const bool flag = DT == DT_I8 && args.split_k > 1 && args.reduce_in_kernel == REDUCE_ATOMIC_FLAG;
     const int flag_tile = tm * args.tiles_n + tn;
@@ -294,7 +294,7 @@ void gemm_ring_kernel(KernelArgs args) {
         ring_barrier<(NB - 2) * LPS + LB>();
         load_frags(I0{}, I0{}, I0{});
         for (int kt = 0; kt < ns; kt += NB) {
-            if (kt == poll_kt) seen = load_coherent(&args.counters[flag_tile * kFlagCounterStride]);
+            if (kt == poll_kt) seen = load_coherent(flag_counter(args, flag_tile));
             static_for<0, NB>([&](auto u) {
                 if (kt + decltype(u)::value < ns) slot(kt + decltype(u)::value, u);
             });

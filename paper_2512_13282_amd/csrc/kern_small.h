@@ -384,7 +384,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
     if (k0 < k_end) load_batch(b0, k0);
     for (; k0 < k_end; k0 += 2 * STEP) {
         if (poll_pending && k0 >= k_poll) {
-            seen = load_coherent(&args.counters[tn * kFlagCounterStride]);
+            seen = load_coherent(flag_counter(args, tn));
             poll_pending = false;
         }
         if (k0 + STEP < k_end) load_batch(b1, k0 + STEP);
@@ -393,7 +393,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(KernelArgs args) {
         if (k0 + 2 * STEP < k_end) load_batch(b0, k0 + 2 * STEP);
         use_batch(b1);
     }
-    if (poll_pending) seen = load_coherent(&args.counters[tn * kFlagCounterStride]);
+    if (poll_pending) seen = load_coherent(flag_counter(args, tn));
 
     // The four waves' partial sums of the same columns, added in wave order.
     __shared__ acc_t red[4][CB];
@@ -477,7 +477,7 @@ __global__ __launch_bounds__(256) void gemv_bt_kernel(KernelArgs args) {
     const int half = int((k_end - k_begin) / (64 * VECE) / 2);
     int64_t k = k_begin + int64_t(lane) * VECE;
     for (int it = 0; it < half; ++it, k += 64 * VECE) step(k);
-    if (flag && slice != 0) seen = load_coherent(&args.counters[tn * kFlagCounterStride]);
+    if (flag && slice != 0) seen = load_coherent(flag_counter(args, tn));
     for (; k < k_end; k += 64 * VECE) step(k);
     // Butterfly over the 64 lanes: every lane ends with the wave's sums.
 #pragma unroll
