@@ -82,9 +82,14 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
     double red_us = 0.0;
     pl.reduce_in_kernel = REDUCE_SEPARATE;
     if (pl.split_k > 1) {
+        // Measured on the skinny bf16 shapes: the last-slice reduction beats the separate
+        // kernel by 1-2 us at M = 1 and loses by 3-7 us at M = 16 (10-40 us at M = 64):
+        // beside its three dependent round trips it issues the tile's device-coherent
+        // partial stores, which grow with the tile's valid rows, and one workgroup reads
+        // every other slice's partial tile.  The separate kernel is priced as a launch.
         const int64_t rows = std::min<int64_t>(c.bm, p.M), cols = std::min<int64_t>(c.bn, p.N);
-        const double trips = double(ceil_div(rows * ceil_div(cols, 4), 256)) * double(ceil_div(pl.split_k, 16));
-        const double in_kernel_us = trips * chip.round_trip_us;
+        const double in_kernel_us = 2.5 + 0.35 * double(rows) +
+                                    double(pl.split_k - 1) * double(rows * cols) * 4.0 / chip.wg_cold_bytes_per_s * 1e6;
         const double separate_us = chip.launch_us;
         int32_t mode = reduce >= 0 ? reduce
                      : p.dtype == DT_I8 ? ((c.family == FAM_RING || c.family == FAM_GEMV) ? REDUCE_ATOMIC_FLAG
@@ -113,8 +118,13 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
 
     // Memory: compulsory traffic at HBM speed; tile re-reads (Eqs. 6-7 analog)
     // mostly from L2/MALL; split-K partials written and read back once, or added
-    // into C once after C is zeroed.
-    const double a_bytes = double(p.M) * p.K * e, b_bytes = double(p.K) * p.N * e;
+    // into C once after C is zeroed.  Row-major B read in row pieces narrower than a
+    // 128-byte line (64 int8 columns) costs whole lines: each tile's piece is half of a
+    // line whose other half a neighbouring workgroup, often on another XCD, fetches again
+    // (measured: the unsplit 64-column int8 plans at M = 32-64 run 1.3-1.7x the
+    // 128-column ones).
+    const double b_line = (!p.trans_b && c.bn * e < 128) ? 128.0 / double(c.bn * e) : 1.0;
+    const double a_bytes = double(p.M) * p.K * e, b_bytes = double(p.K) * p.N * e * b_line;
     const double c_bytes = double(p.M) * p.N * 4;
     const double a_reads = a_bytes * double(pl.tiles_n);
     const double b_reads = b_bytes * double(pl.tiles_m);
@@ -123,6 +133,15 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
     pl.traffic_bytes = a_reads + b_reads + c_bytes + ws;
     pl.t_mem_us = ((a_bytes + b_bytes + c_bytes + ws) / chip.hbm_bytes_per_s +
                    (a_reads + b_reads - a_bytes - b_bytes) / chip.reread_bytes_per_s) * 1e6;
+    // With one tile row every workgroup streams a strip of B of its own from HBM, beside
+    // its slice of A, at a rate one workgroup's loads in flight bound: too few workgroups
+    // cannot reach the HBM rate (measured: 112 unsplit workgroups of 32 x 128 at M = 16
+    // take 1.4x the time of 224 split ones).
+    if (pl.tiles_m == 1 && p.K > 0) {
+        const double wg_bytes = double(std::min<int64_t>(pl.k_chunk, p.K)) *
+                                (double(std::min<int64_t>(c.bm, p.M)) + double(std::min<int64_t>(c.bn, p.N)) * b_line) * e;
+        pl.t_mem_us = std::max(pl.t_mem_us, double(rounds) * wg_bytes / chip.wg_cold_bytes_per_s * 1e6);
+    }
 
     pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + chip.launch_us + red_us;
     return pl;

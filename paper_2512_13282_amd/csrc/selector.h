@@ -35,6 +35,8 @@ struct Chip {
     double  bf16_ops_per_clk_cu = 4096.0; // dense bf16 MFMA
     double  hbm_bytes_per_s = 4.0e12;     // sustained cold-HBM streaming rate the kernels reach
     double  reread_bytes_per_s = 16.0e12; // A/B tile re-reads mostly served by L2/MALL
+    double  wg_cold_bytes_per_s = 30.0e9; // one workgroup streaming its own strip of B from HBM
+                                          // (measured 26-38 GB/s: its loads in flight over the latency)
     double  launch_us = 5.0;              // per kernel launch on the stream
     double  round_trip_us = 1.5;          // one dependent global-memory round trip of a workgroup
 };
