@@ -98,9 +98,10 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
         if ((mode == REDUCE_ATOMIC || mode == REDUCE_ATOMIC_FLAG) && p.dtype != DT_I8) mode = REDUCE_SEPARATE;
         if (mode == REDUCE_ATOMIC_FLAG && c.family != FAM_RING && c.family != FAM_GEMV) mode = REDUCE_ATOMIC;
         pl.reduce_in_kernel = mode;
-        // atomic: the fill launch; atomic with slice 0's zeros: their round trip
+        // atomic: the fill launch; atomic with slice 0's zeros: their round trip, growing
+        // with the slices that add into the same lines of C
         red_us = mode == REDUCE_LAST_SLICE ? in_kernel_us
-               : mode == REDUCE_ATOMIC_FLAG ? chip.round_trip_us : separate_us;
+               : mode == REDUCE_ATOMIC_FLAG ? chip.round_trip_us * (1.0 + double(pl.split_k) / 8.0) : separate_us;
     }
     const bool partial_planes =
         pl.split_k > 1 && pl.reduce_in_kernel != REDUCE_ATOMIC && pl.reduce_in_kernel != REDUCE_ATOMIC_FLAG;
@@ -143,7 +144,11 @@ Plan evaluate(const Problem &p, int32_t cfg, int32_t split, const Chip &chip, in
         pl.t_mem_us = std::max(pl.t_mem_us, double(rounds) * wg_bytes / chip.wg_cold_bytes_per_s * 1e6);
     }
 
-    pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + chip.launch_us + red_us;
+    // Each round of workgroups also pays its tiles' prologue and epilogue (measured at
+    // 2048^3: 1.3 us of first loads and 2.5 us of C stores around an 8.5 us K loop); two
+    // workgroups resident on a CU overlap each other's.
+    pl.t_total_us = std::max(pl.t_comp_us, pl.t_mem_us) + double(rounds) * chip.tile_overhead_us / c.occupancy +
+                    chip.launch_us + red_us;
     return pl;
 }
 

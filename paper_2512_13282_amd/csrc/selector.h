@@ -39,6 +39,8 @@ struct Chip {
                                           // (measured 26-38 GB/s: its loads in flight over the latency)
     double  launch_us = 5.0;              // per kernel launch on the stream
     double  round_trip_us = 1.5;          // one dependent global-memory round trip of a workgroup
+    double  tile_overhead_us = 2.0;       // per round of workgroups: the first loads' latency and
+                                          // the C stores, which the K loop does not hide
 };
 
 int32_t elem_bytes(int32_t dtype);
