@@ -67,5 +67,7 @@ RECT = [(d, M, K, N) for d in DTYPES for (M, K, N) in ((2048, 4096, 11008), (204
 SKINNY = [(d, M, K, N) for d in DTYPES for M in (1, 16, 64) for (K, N) in ((4096, 14336), (14336, 4096))]
 SMALL = [("int8", 256, 256, 256), ("bf16", 1024, 1024, 1024)]
 ALL_CONFIGS = SMALL + SQUARE + RECT + SKINNY
-# Decode batch sizes between the skinny workloads' 1, 16 and 64 rows, for the plan tuner.
-DECODE = [(d, M, K, N) for d in DTYPES for M in (8, 32) for (K, N) in ((4096, 14336), (14336, 4096))]
+# For the plan tuner: decode batch sizes between the skinny workloads' 1, 16 and 64 rows,
+# and the skinny rows at the rectangle workloads' layer dimensions.
+DECODE = ([(d, M, K, N) for d in DTYPES for M in (8, 32) for (K, N) in ((4096, 14336), (14336, 4096))] +
+          [(d, M, K, N) for d in DTYPES for M in (1, 16, 64) for (K, N) in ((4096, 11008), (11008, 4096), (4096, 12288))])
