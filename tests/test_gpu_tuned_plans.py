@@ -1,0 +1,64 @@
+"""Every measured plan of the skinny and decode shapes, run at its own shape (needs an
+MI355X).
+
+The tuned plan table maps exact shapes to (configuration, split, reduction); these are
+the plans a caller of those shapes gets.  Each one is run through the C ABI with the
+selector's own choice (no override), on seeded inputs, and the whole C is compared with
+the oracle: int8 element by element, bf16 by the normalised error.  Larger shapes of the
+table are the benchmark's workloads, covered at full size by the parity tests of each B
+layout.
+"""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2512_13282_amd import binding as b
+from paper_2512_13282_amd import inputs
+import gpu_helpers as g
+
+pytestmark = pytest.mark.gpu
+I8, BF = g.I8, g.BF
+
+
+def _entries():
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "paper_2512_13282_amd", "csrc", "tuned_plans.inc")
+    out = []
+    for line in open(path):
+        m = re.match(r"\s*\{(\d+), (\d+), (\d+), (\d+), (\d+), (\d+), (-?\d+), ([01])\},", line)
+        if m:
+            out.append(tuple(int(x) for x in m.groups()))
+    return out
+
+
+SKINNY_ENTRIES = [e for e in _entries() if e[1] <= 64]
+
+
+@pytest.fixture(autouse=True)
+def _reset_plan():
+    g.unforce()
+    yield
+    g.unforce()
+
+
+def test_table_has_skinny_entries():
+    assert len(SKINNY_ENTRIES) >= 40
+
+
+@pytest.mark.parametrize("entry", SKINNY_ENTRIES,
+                         ids=[f"{'i8' if e[0] == I8 else 'bf16'}-{e[1]}x{e[3]}x{e[2]}{'-bt' if e[7] else ''}"
+                              for e in SKINNY_ENTRIES])
+def test_tuned_plan_at_its_shape(entry):
+    d, M, N, K, cfg, split, reduce, bt = entry
+    fake = 1 << 40
+    plan = b.gemm_plan(d, M, N, K, K, K if bt else N, N, fake, 2 * fake, 3 * fake, trans_b=bool(bt))
+    assert plan["config"] == cfg and plan["split_k"] == split, plan
+    if reduce >= 0 and split > 1:
+        assert plan["reduce_in_kernel"] == reduce, plan
+    print(f"tuned dtype={d} M={M} K={K} N={N} bt={bt} plan={plan['name']} split={split} "
+          f"reduce={plan['reduce_in_kernel']}", flush=True)
+    A, B = inputs.make_inputs("int8" if d == I8 else "bf16", M, N, K, seed=M + N + K)
+    C = g.gemm_gpu_bt(d, A, np.ascontiguousarray(B.T)) if bt else g.gemm_gpu(d, A, B)
+    (g.check_i8 if d == I8 else g.check_bf16)(A, B, np.ascontiguousarray(C))
