@@ -178,12 +178,42 @@ bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *redu
     return false;
 }
 
+// A skinny shape with no measured plan of its own borrows the plan measured for the
+// nearest M at the same dtype, B layout, N and K: such shapes are bound by reading B,
+// whose cost does not depend on M while the number of tile rows, and with it the grid
+// and the reads of B, stays the same.  Only plans whose tile covers the same number of
+// rows of C at both sizes qualify; among them the nearest M on a log scale, the larger
+// on a tie.  The split-K reduction is left to the model, whose price for it grows with
+// the rows summed (at M = 1-4 the in-kernel sum wins over the separate kernel that a
+// plan measured at M = 16 may have used).
+bool neighbour_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce) {
+    if (p.M < 1 || p.M > kNeighbourMaxM) return false;
+    const TunedPlan *best = nullptr;
+    double best_d = 0.0;
+    for (const TunedPlan &t : kTuned) {
+        if (t.dtype != p.dtype || t.trans_b != p.trans_b || t.N != p.N || t.K != p.K) continue;
+        if (t.M < 1 || t.M > kNeighbourMaxM || t.config < 0 || t.config >= kNumConfigs) continue;
+        const int64_t bm = kConfigs[t.config].bm;
+        if ((t.M + bm - 1) / bm != (p.M + bm - 1) / bm || !config_applicable(p, t.config)) continue;
+        const double d = std::fabs(std::log(double(t.M) / double(p.M)));
+        if (!best || d < best_d - 1e-12 || (d <= best_d + 1e-12 && t.M > best->M)) {
+            best = &t;
+            best_d = d;
+        }
+    }
+    if (!best) return false;
+    *config = best->config;
+    *split = best->split;
+    *reduce = -1;
+    return true;
+}
+
 bool select_plan(const Problem &p, Plan *out, int32_t forced_family, int32_t forced_config,
                  int32_t forced_split, const Chip &chip, int32_t forced_reduce) {
     static const int32_t kSplits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64};
     if (forced_family < 0 && forced_config < 0 && forced_split <= 0 && forced_reduce < 0) {
         int32_t cfg, split, reduce;
-        if (tuned_plan(p, &cfg, &split, &reduce)) {
+        if (tuned_plan(p, &cfg, &split, &reduce) || neighbour_plan(p, &cfg, &split, &reduce)) {
             *out = evaluate(p, cfg, split, chip, reduce);
             return true;
         }

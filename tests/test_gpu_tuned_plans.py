@@ -1,12 +1,13 @@
-"""Every measured plan of the skinny and decode shapes, run at its own shape (needs an
-MI355X).
+"""Every measured plan of the skinny and decode shapes, run at its own shape, and the
+plans that other row counts borrow from them (needs an MI355X).
 
 The tuned plan table maps exact shapes to (configuration, split, reduction); these are
-the plans a caller of those shapes gets.  Each one is run through the C ABI with the
-selector's own choice (no override), on seeded inputs, and the whole C is compared with
-the oracle: int8 element by element, bf16 by the normalised error.  Larger shapes of the
-table are the benchmark's workloads, covered at full size by the parity tests of each B
-layout.
+the plans a caller of those shapes gets, and a skinny shape without a plan of its own at
+the same N and K borrows the one of the nearest tuned M.  Each is run through the C ABI
+with the selector's own choice (no override), on seeded inputs, and the whole C is
+compared with the oracle: int8 element by element, bf16 by the normalised error.  Larger
+shapes of the table are the benchmark's workloads, covered at full size by the parity
+tests of each B layout.
 """
 import os
 import re
@@ -34,6 +35,9 @@ def _entries():
 
 
 SKINNY_ENTRIES = [e for e in _entries() if e[1] <= 64]
+# (dtype, M, N, K, B layout) at each tuned (dtype, layout, N, K), for row counts without a plan
+BORROWED = sorted({(e[0], M, e[2], e[3], e[7]) for e in SKINNY_ENTRIES for M in (3, 12, 40)} -
+                  {(e[0], e[1], e[2], e[3], e[7]) for e in SKINNY_ENTRIES})
 
 
 @pytest.fixture(autouse=True)
@@ -60,5 +64,19 @@ def test_tuned_plan_at_its_shape(entry):
     print(f"tuned dtype={d} M={M} K={K} N={N} bt={bt} plan={plan['name']} split={split} "
           f"reduce={plan['reduce_in_kernel']}", flush=True)
     A, B = inputs.make_inputs("int8" if d == I8 else "bf16", M, N, K, seed=M + N + K)
+    C = g.gemm_gpu_bt(d, A, np.ascontiguousarray(B.T)) if bt else g.gemm_gpu(d, A, B)
+    (g.check_i8 if d == I8 else g.check_bf16)(A, B, np.ascontiguousarray(C))
+
+
+@pytest.mark.parametrize("shape", BORROWED,
+                         ids=[f"{'i8' if s[0] == I8 else 'bf16'}-{s[1]}x{s[3]}x{s[2]}{'-bt' if s[4] else ''}"
+                              for s in BORROWED])
+def test_borrowed_plan(shape):
+    d, M, N, K, bt = shape
+    fake = 1 << 40
+    plan = b.gemm_plan(d, M, N, K, K, K if bt else N, N, fake, 2 * fake, 3 * fake, trans_b=bool(bt))
+    print(f"borrowed dtype={d} M={M} K={K} N={N} bt={bt} plan={plan['name']} split={plan['split_k']} "
+          f"reduce={plan['reduce_in_kernel']}", flush=True)
+    A, B = inputs.make_inputs("int8" if d == I8 else "bf16", M, N, K, seed=M + N + K + 1)
     C = g.gemm_gpu_bt(d, A, np.ascontiguousarray(B.T)) if bt else g.gemm_gpu(d, A, B)
     (g.check_i8 if d == I8 else g.check_bf16)(A, B, np.ascontiguousarray(C))

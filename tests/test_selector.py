@@ -1,5 +1,6 @@
 """The shape-driven selector (pure host code, exercised through gemm_plan)."""
 import itertools
+import math
 
 import pytest
 
@@ -149,6 +150,32 @@ def test_tuned_plans_are_valid_and_used():
             assert p["reduce_in_kernel"] == reduce
         assert p["kernel"] != b.GEMM_KERNEL_GENERIC
         check_invariants(p, d, M, N, K)
+
+
+def test_skinny_shapes_borrow_the_nearest_tuned_plan():
+    """M <= 64 without a plan of its own, at a (dtype, B layout, N, K) that has tuned plans:
+    the configuration and split of the tuned plan with the nearest M on a log scale (the
+    larger M on a tie) among those whose tile covers as many tile rows at both sizes."""
+    groups = {}
+    for (d, M, N, K, cfg, split, reduce, bt) in _tuned_entries():
+        if M <= 64:
+            groups.setdefault((d, bt, N, K), {})[M] = (cfg, split)
+    checked = 0
+    for (d, bt, N, K), by_m in groups.items():
+        pl = plan_bt if bt else plan
+        bm = {m: pl(d, m, N, K)["bm"] for m in by_m}
+        for M in range(1, 65):
+            if M in by_m:
+                continue
+            p = pl(d, M, N, K)
+            check_invariants(p, d, M, N, K)
+            same_rows = [m for m in by_m if -(-m // bm[m]) == -(-M // bm[m])]
+            if not same_rows:
+                continue
+            near = min(same_rows, key=lambda m: (abs(math.log(m / M)), -m))
+            assert (p["config"], p["split_k"]) == by_m[near], (d, bt, M, N, K, p["name"], near)
+            checked += 1
+    assert checked >= 1000
 
 
 def test_tuned_plans_skip_misaligned_operands():
