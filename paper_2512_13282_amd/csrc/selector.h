@@ -64,11 +64,11 @@ bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *redu
 // For M <= kNeighbourMaxM without a plan of its own: the plan measured for the nearest
 // tuned M (same dtype, B layout, N and K, same number of tile rows), if any, with
 // *reduce = -1 (the model picks the reduction).
-constexpr int64_t kNeighbourMaxM = 64;
+constexpr int64_t kNeighbourMaxM = 256;
 bool neighbour_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce);
 
-// Best plan: a tuned plan for this exact shape if one applies, else a skinny
-// neighbour's tuned plan, else the model's.  forced_family < 0 means any family; forced_config
+// Best plan: a tuned plan for this exact shape if one applies, else a neighbour's
+// tuned plan (M <= kNeighbourMaxM), else the model's.  forced_family < 0 means any family; forced_config
 // >= 0 pins the configuration; forced_split > 0 pins the split factor.
 // Returns false if nothing applicable exists (only possible when forced).
 // forced_reduce >= 0 pins the split-K reduction (0 separate kernel, 1 in-kernel).

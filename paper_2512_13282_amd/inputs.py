@@ -21,10 +21,15 @@ DTYPES = ("int8", "bf16")
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bf16 (nearest, ties to even); uint16 bits out.  Infinities
     keep their sign; a NaN stays a NaN (its upper half with the quiet bit set)."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    nan = (u & 0x7FFFFFFF) > 0x7F800000
-    return np.where(nan, (u >> 16) | 0x40, r).astype(np.uint16)
+    # In uint32: the sum stays below 2^32 for every non-NaN pattern (at most
+    # 0xFF800000 + 0x8000); NaN sums may wrap, and are replaced.
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    one, half = np.uint32(1), np.uint32(0x7FFF)
+    r = ((u + half + ((u >> np.uint32(16)) & one)) >> np.uint32(16)).astype(np.uint16)
+    nan = (u & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+    if nan.any():
+        r[nan] = ((u[nan] >> np.uint32(16)) | np.uint32(0x40)).astype(np.uint16)
+    return r
 
 
 def f32_from_bf16_bits(b: np.ndarray) -> np.ndarray:
@@ -68,6 +73,9 @@ SKINNY = [(d, M, K, N) for d in DTYPES for M in (1, 16, 64) for (K, N) in ((4096
 SMALL = [("int8", 256, 256, 256), ("bf16", 1024, 1024, 1024)]
 ALL_CONFIGS = SMALL + SQUARE + RECT + SKINNY
 # For the plan tuner: decode batch sizes between the skinny workloads' 1, 16 and 64 rows,
-# and the skinny rows at the rectangle workloads' layer dimensions.
-DECODE = ([(d, M, K, N) for d in DTYPES for M in (8, 32) for (K, N) in ((4096, 14336), (14336, 4096))] +
-          [(d, M, K, N) for d in DTYPES for M in (1, 16, 64) for (K, N) in ((4096, 11008), (11008, 4096), (4096, 12288))])
+# the skinny rows at the rectangle workloads' layer dimensions, and short prefill chunks
+# (128 and 256 rows) at all five layer dimensions.
+LAYER_KN = ((4096, 14336), (14336, 4096), (4096, 11008), (11008, 4096), (4096, 12288))
+DECODE = ([(d, M, K, N) for d in DTYPES for M in (8, 32) for (K, N) in LAYER_KN[:2]] +
+          [(d, M, K, N) for d in DTYPES for M in (1, 16, 32, 64) for (K, N) in LAYER_KN[2:]])
+PREFILL = [(d, M, K, N) for d in DTYPES for M in (128, 256) for (K, N) in LAYER_KN]

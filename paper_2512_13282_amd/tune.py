@@ -222,8 +222,9 @@ def main():
     sys.path.insert(0, os.path.dirname(PKG))
     from . import inputs
     if args.shapes == "default":
-        shapes = [tuple(s) for s in inputs.ALL_CONFIGS + inputs.DECODE]
-        shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + inputs.DECODE + [c for c in inputs.SQUARE if c[1] == 8192]]
+        shapes = [tuple(s) for s in inputs.ALL_CONFIGS + inputs.DECODE + inputs.PREFILL]
+        shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + inputs.DECODE + inputs.PREFILL +
+                   [c for c in inputs.SQUARE if c[1] == 8192]]
     else:
         shapes = [tuple(s) for s in json.load(open(args.shapes))]
     entries, everything = [], []

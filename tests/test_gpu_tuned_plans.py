@@ -1,9 +1,10 @@
-"""Every measured plan of the skinny and decode shapes, run at its own shape, and the
-plans that other row counts borrow from them (needs an MI355X).
+"""Every measured plan of the skinny, decode and short prefill shapes (M <= 256), run at
+its own shape, and the plans that other row counts up to 256 borrow from them (needs an
+MI355X).
 
 The tuned plan table maps exact shapes to (configuration, split, reduction); these are
-the plans a caller of those shapes gets, and a skinny shape without a plan of its own at
-the same N and K borrows the one of the nearest tuned M.  Each is run through the C ABI
+the plans a caller of those shapes gets, and a shape with M <= 256 and no plan of its own
+at the same N and K borrows the one of the nearest tuned M.  Each is run through the C ABI
 with the selector's own choice (no override), on seeded inputs, and the whole C is
 compared with the oracle: int8 element by element, bf16 by the normalised error.  Larger
 shapes of the table are the benchmark's workloads, covered at full size by the parity
@@ -34,10 +35,12 @@ def _entries():
     return out
 
 
-SKINNY_ENTRIES = [e for e in _entries() if e[1] <= 64]
-# (dtype, M, N, K, B layout) at each tuned (dtype, layout, N, K), for row counts without a plan
-BORROWED = sorted({(e[0], M, e[2], e[3], e[7]) for e in SKINNY_ENTRIES for M in (3, 12, 40)} -
-                  {(e[0], e[1], e[2], e[3], e[7]) for e in SKINNY_ENTRIES})
+TABLE_ENTRIES = [e for e in _entries() if e[1] <= 256]
+# (dtype, M, N, K, B layout) at each (dtype, layout, N, K) with skinny tuned plans, for row
+# counts without a plan of their own
+_GROUPS = {(e[0], e[2], e[3], e[7]) for e in TABLE_ENTRIES if e[1] <= 64}
+BORROWED = sorted({(d, M, N, K, bt) for (d, N, K, bt) in _GROUPS for M in (3, 12, 40, 96, 192)} -
+                  {(e[0], e[1], e[2], e[3], e[7]) for e in TABLE_ENTRIES})
 
 
 @pytest.fixture(autouse=True)
@@ -47,13 +50,13 @@ def _reset_plan():
     g.unforce()
 
 
-def test_table_has_skinny_entries():
-    assert len(SKINNY_ENTRIES) >= 40
+def test_table_has_short_entries():
+    assert sum(e[1] <= 64 for e in TABLE_ENTRIES) >= 40 and len(_GROUPS) >= 20
 
 
-@pytest.mark.parametrize("entry", SKINNY_ENTRIES,
+@pytest.mark.parametrize("entry", TABLE_ENTRIES,
                          ids=[f"{'i8' if e[0] == I8 else 'bf16'}-{e[1]}x{e[3]}x{e[2]}{'-bt' if e[7] else ''}"
-                              for e in SKINNY_ENTRIES])
+                              for e in TABLE_ENTRIES])
 def test_tuned_plan_at_its_shape(entry):
     d, M, N, K, cfg, split, reduce, bt = entry
     fake = 1 << 40
