@@ -74,8 +74,12 @@ SMALL = [("int8", 256, 256, 256), ("bf16", 1024, 1024, 1024)]
 ALL_CONFIGS = SMALL + SQUARE + RECT + SKINNY
 # For the plan tuner: decode batch sizes between the skinny workloads' 1, 16 and 64 rows,
 # the skinny rows at the rectangle workloads' layer dimensions, and short prefill chunks
-# (128 and 256 rows) at all five layer dimensions.
+# (128 and 256 rows) at all five layer dimensions; then the same row counts at further
+# transformer projection sizes (K = hidden size 4096 or 8192; N = the fused query/key/value
+# width, the hidden size, or the feed-forward width, and the transposed feed-forward shape).
 LAYER_KN = ((4096, 14336), (14336, 4096), (4096, 11008), (11008, 4096), (4096, 12288))
 DECODE = ([(d, M, K, N) for d in DTYPES for M in (8, 32) for (K, N) in LAYER_KN[:2]] +
           [(d, M, K, N) for d in DTYPES for M in (1, 16, 32, 64) for (K, N) in LAYER_KN[2:]])
 PREFILL = [(d, M, K, N) for d in DTYPES for M in (128, 256) for (K, N) in LAYER_KN]
+MORE_LAYER_KN = ((4096, 6144), (4096, 4096), (8192, 28672), (28672, 8192), (8192, 10240), (8192, 8192))
+MORE_LAYERS = [(d, M, K, N) for (K, N) in MORE_LAYER_KN for d in DTYPES for M in (1, 16, 64, 128, 256)]

@@ -222,9 +222,9 @@ def main():
     sys.path.insert(0, os.path.dirname(PKG))
     from . import inputs
     if args.shapes == "default":
-        shapes = [tuple(s) for s in inputs.ALL_CONFIGS + inputs.DECODE + inputs.PREFILL]
+        shapes = [tuple(s) for s in inputs.ALL_CONFIGS + inputs.DECODE + inputs.PREFILL + inputs.MORE_LAYERS]
         shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + inputs.DECODE + inputs.PREFILL +
-                   [c for c in inputs.SQUARE if c[1] == 8192]]
+                   inputs.MORE_LAYERS + [c for c in inputs.SQUARE if c[1] == 8192]]
     else:
         shapes = [tuple(s) for s in json.load(open(args.shapes))]
     entries, everything = [], []

@@ -1,21 +1,23 @@
-"""Every measured plan of the skinny, decode and short prefill shapes (M <= 256), run at
-its own shape, and the plans that other row counts up to 256 borrow from them (needs an
-MI355X).
+"""Every measured plan of the decode and short prefill shapes (M <= 256), run at its own
+shape, and the plans that other row counts up to 256 borrow from them (needs an MI355X).
 
 The tuned plan table maps exact shapes to (configuration, split, reduction); these are
 the plans a caller of those shapes gets, and a shape with M <= 256 and no plan of its own
 at the same N and K borrows the one of the nearest tuned M.  Each is run through the C ABI
-with the selector's own choice (no override), on seeded inputs, and the whole C is
-compared with the oracle: int8 element by element, bf16 by the normalised error.  Larger
-shapes of the table are the benchmark's workloads, covered at full size by the parity
-tests of each B layout.
+with the selector's own choice (no override), on seeded inputs, and compared with the
+oracle: int8 element by element, bf16 by the normalised error; the whole C up to 64 rows,
+sampled rows above (int8 also by Freivalds' test over the whole C).  Larger shapes of the
+table are the benchmark's workloads, covered at full size by the parity tests of each B
+layout.  Tests of one (dtype, K, N) run back to back and share one B.
 """
+import functools
 import os
 import re
 
 import numpy as np
 import pytest
 
+from oracle import oracle
 from paper_2512_13282_amd import binding as b
 from paper_2512_13282_amd import inputs
 import gpu_helpers as g
@@ -35,12 +37,14 @@ def _entries():
     return out
 
 
-TABLE_ENTRIES = [e for e in _entries() if e[1] <= 256]
+_order = lambda e: (e[0], e[3], e[2], e[-1], e[1])     # dtype, K, N, layout, M
+TABLE_ENTRIES = sorted((e for e in _entries() if e[1] <= 256), key=_order)
 # (dtype, M, N, K, B layout) at each (dtype, layout, N, K) with skinny tuned plans, for row
 # counts without a plan of their own
 _GROUPS = {(e[0], e[2], e[3], e[7]) for e in TABLE_ENTRIES if e[1] <= 64}
 BORROWED = sorted({(d, M, N, K, bt) for (d, N, K, bt) in _GROUPS for M in (3, 12, 40, 96, 192)} -
-                  {(e[0], e[1], e[2], e[3], e[7]) for e in TABLE_ENTRIES})
+                  {(e[0], e[1], e[2], e[3], e[7]) for e in TABLE_ENTRIES}, key=_order)
+FULL_ROWS = 64
 
 
 @pytest.fixture(autouse=True)
@@ -48,6 +52,36 @@ def _reset_plan():
     g.unforce()
     yield
     g.unforce()
+
+
+@functools.lru_cache(maxsize=1)
+def _b(d, K, N):
+    """B (K x N) of one (dtype, K, N), and its transpose, drawn once for the tests that share it."""
+    B = (inputs.int8_matrix if d == I8 else inputs.bf16_matrix)(K, N, seed=1 + K + N)
+    return B, np.ascontiguousarray(B.T)
+
+
+def _run_and_check(d, M, N, K, bt, seed):
+    fake = 1 << 40
+    plan = b.gemm_plan(d, M, N, K, K, K if bt else N, N, fake, 2 * fake, 3 * fake, trans_b=bool(bt))
+    print(f"dtype={d} M={M} K={K} N={N} bt={bt} plan={plan['name']} split={plan['split_k']} "
+          f"reduce={plan['reduce_in_kernel']}", flush=True)
+    A = (inputs.int8_matrix if d == I8 else inputs.bf16_matrix)(M, K, seed=seed)
+    B, Bt = _b(d, K, N)
+    C = np.ascontiguousarray(g.gemm_gpu_bt(d, A, Bt) if bt else g.gemm_gpu(d, A, B))
+    if M <= FULL_ROWS:
+        (g.check_i8 if d == I8 else g.check_bf16)(A, B, C)
+        return plan
+    rng = np.random.default_rng(seed)
+    rows = sorted({0, M // 2, M - 1} | {int(r) for r in rng.integers(0, M, size=5)})
+    Ar = np.ascontiguousarray(A[rows])
+    if d == I8:
+        assert oracle.get().freivalds_i8_i32(A, B, C, trials=2) == 0
+        g.check_i8(Ar, B, np.ascontiguousarray(C[rows]))
+    else:
+        assert np.all(np.isfinite(C))
+        g.check_bf16(Ar, B, np.ascontiguousarray(C[rows]))
+    return plan
 
 
 def test_table_has_short_entries():
@@ -59,16 +93,10 @@ def test_table_has_short_entries():
                               for e in TABLE_ENTRIES])
 def test_tuned_plan_at_its_shape(entry):
     d, M, N, K, cfg, split, reduce, bt = entry
-    fake = 1 << 40
-    plan = b.gemm_plan(d, M, N, K, K, K if bt else N, N, fake, 2 * fake, 3 * fake, trans_b=bool(bt))
+    plan = _run_and_check(d, M, N, K, bt, seed=M)
     assert plan["config"] == cfg and plan["split_k"] == split, plan
     if reduce >= 0 and split > 1:
         assert plan["reduce_in_kernel"] == reduce, plan
-    print(f"tuned dtype={d} M={M} K={K} N={N} bt={bt} plan={plan['name']} split={split} "
-          f"reduce={plan['reduce_in_kernel']}", flush=True)
-    A, B = inputs.make_inputs("int8" if d == I8 else "bf16", M, N, K, seed=M + N + K)
-    C = g.gemm_gpu_bt(d, A, np.ascontiguousarray(B.T)) if bt else g.gemm_gpu(d, A, B)
-    (g.check_i8 if d == I8 else g.check_bf16)(A, B, np.ascontiguousarray(C))
 
 
 @pytest.mark.parametrize("shape", BORROWED,
@@ -76,10 +104,4 @@ def test_tuned_plan_at_its_shape(entry):
                               for s in BORROWED])
 def test_borrowed_plan(shape):
     d, M, N, K, bt = shape
-    fake = 1 << 40
-    plan = b.gemm_plan(d, M, N, K, K, K if bt else N, N, fake, 2 * fake, 3 * fake, trans_b=bool(bt))
-    print(f"borrowed dtype={d} M={M} K={K} N={N} bt={bt} plan={plan['name']} split={plan['split_k']} "
-          f"reduce={plan['reduce_in_kernel']}", flush=True)
-    A, B = inputs.make_inputs("int8" if d == I8 else "bf16", M, N, K, seed=M + N + K + 1)
-    C = g.gemm_gpu_bt(d, A, np.ascontiguousarray(B.T)) if bt else g.gemm_gpu(d, A, B)
-    (g.check_i8 if d == I8 else g.check_bf16)(A, B, np.ascontiguousarray(C))
+    _run_and_check(d, M, N, K, bt, seed=M + 1)
