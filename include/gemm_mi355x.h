@@ -250,6 +250,28 @@ int gemm_plan_bt(int dtype, int64_t M, int64_t N, int64_t K,
  * unknown kernel/config or a split factor < 0. */
 int gemm_force_plan(int dtype, int kernel, int config, int split_k);
 
+/* Measured plans loaded at run time: the on-device measurement step of the
+ * paper's tiling search (Sec. 4.5.2) without rebuilding the library.  `path`
+ * names a text file with one plan per line, eight decimal integers separated by
+ * blanks -- dtype M N K config split_k reduce trans_b -- the fields of the
+ * compiled plan table (reduce: a GEMM_REDUCE_* value, or -1 for the selector's
+ * choice; trans_b: 1 for the *_bt calls); '#' starts a comment that runs to the
+ * end of the line.  `python -m paper_2512_13282_amd.tune --plans-out FILE`
+ * writes this format.  For exactly those shapes and B layouts the loaded plans
+ * take precedence over the compiled table and the model, in this process; a
+ * call whose operands the plan's configuration cannot run (alignment) uses the
+ * selector's plan as before.  A later line, or a later load, for the same shape
+ * replaces an earlier one.  The environment variable GEMM_MI355X_PLANS, if set,
+ * names a file loaded the same way before the first plan is chosen (a file that
+ * does not load is reported once on stderr and ignored).  The path is only read
+ * during the call.  Not thread-safe with respect to concurrent GEMM calls.
+ * Returns GEMM_OK, or GEMM_ERR_INVALID_VALUE (NULL path, unreadable file, a
+ * malformed or out-of-range line: then nothing is loaded). */
+int gemm_load_plans(const char *path);
+
+/* Drops every plan loaded by gemm_load_plans or GEMM_MI355X_PLANS.  Returns GEMM_OK. */
+int gemm_clear_plans(void);
+
 /* Frees the split-K workspaces the library holds (every device and stream).
  * Synchronizes each device that holds one first, so it must not be called while
  * another thread is issuing GEMM calls; later split-K calls allocate afresh.

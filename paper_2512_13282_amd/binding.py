@@ -51,7 +51,7 @@ EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt"
             "gemm_bf16_bf16_bt", "gemm_plan",
             "gemm_plan_bt", "gemm_force_plan", "gemm_force_reduce", "gemm_release_workspace",
             "gemm_status_string", "gemm_version", "gemm_probe_mfma", "gemm_bf16_f32_noalloc",
-            "gemm_probe_read")
+            "gemm_probe_read", "gemm_load_plans", "gemm_clear_plans")
 
 
 class PlanInfo(ctypes.Structure):
@@ -122,6 +122,10 @@ def lib() -> ctypes.CDLL:
         l.gemm_force_reduce.restype = i32
         l.gemm_release_workspace.argtypes = []
         l.gemm_release_workspace.restype = i32
+        l.gemm_load_plans.argtypes = [ctypes.c_char_p]
+        l.gemm_load_plans.restype = i32
+        l.gemm_clear_plans.argtypes = []
+        l.gemm_clear_plans.restype = i32
         l.gemm_status_string.argtypes = [i32]
         l.gemm_status_string.restype = ctypes.c_char_p
         l.gemm_version.argtypes = []
@@ -199,6 +203,14 @@ def gemm_force_plan(dtype, kernel=GEMM_KERNEL_AUTO, config=-1, split_k=0) -> int
 
 def gemm_force_reduce(dtype, mode=-1) -> int:
     return lib().gemm_force_reduce(dtype, mode)
+
+
+def gemm_load_plans(path) -> int:
+    return lib().gemm_load_plans(None if path is None else os.fsencode(path))
+
+
+def gemm_clear_plans() -> int:
+    return lib().gemm_clear_plans()
 
 
 def gemm_release_workspace() -> int:

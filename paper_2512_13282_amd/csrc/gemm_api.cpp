@@ -3,11 +3,16 @@
 // Validation happens here, on the host, before any HIP call; the plan comes
 // from the selector (cached per shape/alignment class); the launch goes
 // through launch_gemm (gemm_launch.hip).
+#include <errno.h>
 #include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <mutex>
 #include <unordered_map>
+#include <utility>
+#include <vector>
 
 #include "../../include/gemm_mi355x.h"
 #include "configs.h"
@@ -49,6 +54,88 @@ struct KeyHash {
 };
 std::unordered_map<Key, Plan, KeyHash> g_cache;
 
+// Plans loaded at run time (gemm_load_plans, GEMM_MI355X_PLANS), per exact shape and
+// B layout; they take precedence over the compiled table.  Guarded by g_mu.
+struct Shape {
+    int32_t dtype;
+    int64_t M, N, K;
+    int32_t trans_b;
+    bool operator==(const Shape &o) const {
+        return dtype == o.dtype && M == o.M && N == o.N && K == o.K && trans_b == o.trans_b;
+    }
+};
+struct ShapeHash {
+    size_t operator()(const Shape &s) const { return KeyHash()(Key{s.dtype, s.M, s.N, s.K, false, s.trans_b}); }
+};
+struct LoadedPlan {
+    int32_t config, split, reduce;
+};
+std::unordered_map<Shape, LoadedPlan, ShapeHash> g_loaded;
+std::once_flag g_env_once;
+
+// One field of a plan line: a decimal integer in [lo, hi].  Advances *s past it.
+bool parse_field(char **s, long long lo, long long hi, long long *v) {
+    char *end = nullptr;
+    errno = 0;
+    const long long x = strtoll(*s, &end, 10);
+    if (end == *s || errno != 0 || x < lo || x > hi) return false;
+    *v = x;
+    *s = end;
+    return true;
+}
+
+// Reads a plan file: one plan per line, "dtype M N K config split reduce trans_b" (the
+// fields of the compiled table), '#' to the end of a line is a comment, blank lines
+// are skipped.  All or nothing: any unreadable file, malformed or out-of-range line
+// leaves `out` unused and returns GEMM_ERR_INVALID_VALUE.
+int read_plan_file(const char *path, std::vector<std::pair<Shape, LoadedPlan>> *out) {
+    if (path == nullptr) return GEMM_ERR_INVALID_VALUE;
+    FILE *f = fopen(path, "r");
+    if (f == nullptr) return GEMM_ERR_INVALID_VALUE;
+    const long long kMaxDim = 1LL << 55;
+    char line[512];
+    int rc = GEMM_OK;
+    while (rc == GEMM_OK && fgets(line, sizeof(line), f) != nullptr) {
+        if (strchr(line, '\n') == nullptr && !feof(f)) { rc = GEMM_ERR_INVALID_VALUE; break; }   // too long
+        if (char *hash = strchr(line, '#')) *hash = '\0';
+        char *s = line;
+        while (*s == ' ' || *s == '\t' || *s == '\r' || *s == '\n') ++s;
+        if (*s == '\0') continue;
+        long long v[8];
+        const long long lo[8] = {0, 0, 0, 0, 0, 1, -1, 0};
+        const long long hi[8] = {1, kMaxDim, kMaxDim, kMaxDim, gemm::kNumConfigs - 1, 1 << 20, 3, 1};
+        for (int i = 0; i < 8 && rc == GEMM_OK; ++i)
+            if (!parse_field(&s, lo[i], hi[i], &v[i])) rc = GEMM_ERR_INVALID_VALUE;
+        while (rc == GEMM_OK && (*s == ' ' || *s == '\t' || *s == '\r' || *s == '\n')) ++s;
+        if (rc == GEMM_OK && *s != '\0') rc = GEMM_ERR_INVALID_VALUE;            // trailing text
+        if (rc == GEMM_OK)
+            out->push_back({Shape{int32_t(v[0]), v[1], v[2], v[3], int32_t(v[7])},
+                            LoadedPlan{int32_t(v[4]), int32_t(v[5]), int32_t(v[6])}});
+    }
+    if (ferror(f)) rc = GEMM_ERR_INVALID_VALUE;
+    fclose(f);
+    return rc;
+}
+
+// Adds every plan of the file to the loaded ones (a later line for the same shape wins).
+int load_plan_file(const char *path) {
+    std::vector<std::pair<Shape, LoadedPlan>> plans;
+    const int rc = read_plan_file(path, &plans);
+    if (rc != GEMM_OK) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    for (const auto &kv : plans) g_loaded[kv.first] = kv.second;
+    g_cache.clear();
+    return GEMM_OK;
+}
+
+// GEMM_MI355X_PLANS names a plan file to load before the first plan is chosen.
+void load_env_plans() {
+    const char *path = getenv("GEMM_MI355X_PLANS");
+    if (path == nullptr || *path == '\0') return;
+    if (load_plan_file(path) != GEMM_OK)
+        fprintf(stderr, "gemm_mi355x: GEMM_MI355X_PLANS=%s not loaded (unreadable file or malformed line)\n", path);
+}
+
 bool overlaps(uintptr_t a0, uint64_t alen, uintptr_t b0, uint64_t blen) {
     if (alen == 0 || blen == 0) return false;
     return a0 < b0 + blen && b0 < a0 + alen;
@@ -89,6 +176,7 @@ int validate(const Problem &p, const void *A, const void *B, const void *C, int6
 }
 
 int plan_for(const Problem &p, Plan *out) {
+    std::call_once(g_env_once, load_env_plans);
     Override ov;
     {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -105,7 +193,20 @@ int plan_for(const Problem &p, Plan *out) {
         }
     }
     Plan pl;
-    if (!gemm::select_plan(p, &pl, ov.family, ov.config, ov.split, gemm::Chip(), ov.reduce))
+    bool loaded = false;
+    if (!forced) {
+        LoadedPlan lp{};
+        {
+            std::lock_guard<std::mutex> lk(g_mu);
+            auto it = g_loaded.find(Shape{p.dtype, p.M, p.N, p.K, p.trans_b});
+            loaded = it != g_loaded.end();
+            if (loaded) lp = it->second;
+        }
+        // A loaded plan whose configuration cannot run this call (alignment) is skipped.
+        loaded = loaded && gemm::config_applicable(p, lp.config);
+        if (loaded) pl = gemm::evaluate(p, lp.config, lp.split, gemm::Chip(), lp.reduce);
+    }
+    if (!loaded && !gemm::select_plan(p, &pl, ov.family, ov.config, ov.split, gemm::Chip(), ov.reduce))
         return GEMM_ERR_UNSUPPORTED;
     if (!forced) {
         const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p), p.trans_b};
@@ -297,6 +398,19 @@ int gemm_force_reduce(int dtype, int mode) {
     if (mode < -1 || mode > 3) return GEMM_ERR_INVALID_VALUE;
     std::lock_guard<std::mutex> lk(g_mu);
     g_override[dtype].reduce = mode;
+    return GEMM_OK;
+}
+
+int gemm_load_plans(const char *path) {
+    std::call_once(g_env_once, load_env_plans);
+    return load_plan_file(path);
+}
+
+int gemm_clear_plans(void) {
+    std::call_once(g_env_once, load_env_plans);
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_loaded.clear();
+    g_cache.clear();
     return GEMM_OK;
 }
 

@@ -6,9 +6,11 @@ candidate (configuration, split-K) plans of each shape on the GPU and writes
 the fastest into ``csrc/tuned_plans.inc``, which the selector consults before
 its model for an exactly matching, suitably aligned shape -- the paper's
 procedure of refining the modelled tile choice by measurement on the device
-(Sec. 4.5.2).  Rebuild the library afterwards.
+(Sec. 4.5.2).  Rebuild the library afterwards.  With --plans-out the plans go
+instead to a plan file that gemm_load_plans / GEMM_MI355X_PLANS load at run time,
+no rebuild needed (--out as well writes both).
 
-    python -m paper_2512_13282_amd.tune [--shapes default|FILE] [--out PATH] [--iters N]
+    python -m paper_2512_13282_amd.tune [--shapes default|FILE] [--out PATH] [--plans-out PATH] [--iters N]
 
 Every plan is first timed in a short burst (the median of --iters launches); the
 fastest --confirm plans, plus the fastest of each split-K reduction, are then
@@ -210,10 +212,24 @@ def write_inc(entries, path=OUT):
         f.write("\n".join(lines) + "\n")
 
 
+def write_plan_file(entries, path):
+    """The run-time plan file format of gemm_load_plans: one plan per line,
+    "dtype M N K config split reduce trans_b", '#' comments."""
+    lines = ["# gemm_mi355x plans measured by `python -m paper_2512_13282_amd.tune`",
+             "# dtype M N K config split reduce trans_b"]
+    for e in entries:
+        lines.append(f"{e['dtype']} {e['M']} {e['N']} {e['K']} {e['config']} {e['split']} {e['reduce']} "
+                     f"{e.get('trans_b', 0)}  # {e['name']} {e.get('us_sustained', e['us']):.1f} us")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--shapes", default="default", help="'default' or a JSON file of [dtype, M, K, N] lists")
-    ap.add_argument("--out", default=OUT)
+    ap.add_argument("--out", default=None,
+                    help="compiled plan table to write (default: csrc/tuned_plans.inc, unless --plans-out is given)")
+    ap.add_argument("--plans-out", default=None, help="write the plans as a run-time plan file (gemm_load_plans)")
     ap.add_argument("--json", default=None, help="also write every measurement here")
     ap.add_argument("--iters", type=int, default=15, help="launches per plan in the screening burst")
     ap.add_argument("--confirm", type=int, default=3,
@@ -236,11 +252,15 @@ def main():
         best, res = tune_shape(dtype, M, N, K, args.iters, bt=bt, confirm=args.confirm, cold_single=cold_single)
         entries.append({"dtype": 0 if dtype == "int8" else 1, "M": M, "N": N, "K": K, "trans_b": int(bt), **best})
         everything.append({"dtype": dtype, "M": M, "K": K, "N": N, "bt": bt, "results": res})
-    write_inc(entries, args.out)
+    out = args.out or (None if args.plans_out else OUT)
+    if out:
+        write_inc(entries, out)
+    if args.plans_out:
+        write_plan_file(entries, args.plans_out)
     if args.json:
         with open(args.json, "w") as f:
             json.dump(everything, f)
-    print(f"wrote {args.out} ({len(entries)} shapes)")
+    print(f"wrote {', '.join(p for p in (out, args.plans_out) if p)} ({len(entries)} shapes)")
 
 
 if __name__ == "__main__":

@@ -4,8 +4,8 @@
   every oracle pin runs against that build.
 * The C ABI and the selector (csrc/gemm_api.cpp, csrc/selector.cpp) are rebuilt as a
   host-only library (tests/sanitize_stub.cpp stands in for the device side, which these
-  tests never reach) with the same sanitizers, and the CPU ABI and selector tests run
-  against it.
+  tests never reach) with the same sanitizers, and the CPU ABI, selector and plan-file
+  tests run against it.
 
 Each run is a child Python process with the ASan runtime preloaded; any sanitizer report
 aborts the child and fails the test."""
@@ -65,7 +65,8 @@ def test_c_abi_and_selector_under_sanitizers(tmp_path):
            os.path.join(HERE, "sanitize_stub.cpp"), "-o", out]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-p", "no:cacheprovider", "-m", "not gpu",
-                        os.path.join(HERE, "test_abi_cpu.py"), os.path.join(HERE, "test_selector.py")],
+                        os.path.join(HERE, "test_abi_cpu.py"), os.path.join(HERE, "test_selector.py"),
+                        os.path.join(HERE, "test_plan_file.py")],
                        env=_env({"GEMM_MI355X_LIBRARY": out}), capture_output=True, text=True, timeout=600,
                        cwd=ROOT)
     assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
