@@ -83,3 +83,5 @@ DECODE = ([(d, M, K, N) for d in DTYPES for M in (8, 32) for (K, N) in LAYER_KN[
 PREFILL = [(d, M, K, N) for d in DTYPES for M in (128, 256) for (K, N) in LAYER_KN]
 MORE_LAYER_KN = ((4096, 6144), (4096, 4096), (8192, 28672), (28672, 8192), (8192, 10240), (8192, 8192))
 MORE_LAYERS = [(d, M, K, N) for (K, N) in MORE_LAYER_KN for d in DTYPES for M in (1, 16, 64, 128, 256)]
+# Longer prefill chunks (512 and 2048 rows) at all eleven sizes.
+PREFILL_LONG = [(d, M, K, N) for (K, N) in LAYER_KN + MORE_LAYER_KN for d in DTYPES for M in (512, 2048)]

@@ -1,5 +1,5 @@
-"""Every measured plan of the decode and short prefill shapes (M <= 256), run at its own
-shape, and the plans that other row counts up to 256 borrow from them (needs an MI355X).
+"""Every measured plan of the decode and prefill shapes (M <= 2048), run at its own shape,
+and the plans that other row counts up to 256 borrow from them (needs an MI355X).
 
 The tuned plan table maps exact shapes to (configuration, split, reduction); these are
 the plans a caller of those shapes gets, and a shape with M <= 256 and no plan of its own
@@ -38,7 +38,7 @@ def _entries():
 
 
 _order = lambda e: (e[0], e[3], e[2], e[-1], e[1])     # dtype, K, N, layout, M
-TABLE_ENTRIES = sorted((e for e in _entries() if e[1] <= 256), key=_order)
+TABLE_ENTRIES = sorted((e for e in _entries() if e[1] <= 2048), key=_order)
 # (dtype, M, N, K, B layout) at each (dtype, layout, N, K) with skinny tuned plans, for row
 # counts without a plan of their own
 _GROUPS = {(e[0], e[2], e[3], e[7]) for e in TABLE_ENTRIES if e[1] <= 64}
@@ -85,7 +85,7 @@ def _run_and_check(d, M, N, K, bt, seed):
 
 
 def test_table_has_short_entries():
-    assert sum(e[1] <= 64 for e in TABLE_ENTRIES) >= 40 and len(_GROUPS) >= 20
+    assert sum(e[1] <= 64 for e in TABLE_ENTRIES) >= 40 and len(_GROUPS) >= 20 and len(TABLE_ENTRIES) >= 300
 
 
 @pytest.mark.parametrize("entry", TABLE_ENTRIES,
