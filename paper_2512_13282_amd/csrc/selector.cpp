@@ -178,12 +178,12 @@ bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *redu
     return false;
 }
 
-// A shape with few rows (M <= kNeighbourMaxM) and no measured plan of its own borrows
-// the plan measured for the nearest M at the same dtype, B layout, N and K: at these
-// sizes reading B dominates, and its cost does not depend on M while the number of tile
-// rows, and with it the grid and the reads of B, stays the same.  Only plans whose tile
-// covers the same number of rows of C at both sizes qualify; among them the nearest M
-// on a log scale, the larger on a tie.  The split-K reduction is left to the model,
+// A shape with M <= kNeighbourMaxM and no measured plan of its own borrows the plan
+// measured for the nearest M at the same dtype, B layout, N and K.  Only plans whose
+// tile covers the same number of rows of C at both sizes qualify, so the borrowed plan
+// runs the same grid of tiles over the same reads of B as where it was measured (few
+// rows: reading B is most of the work and does not depend on M; more: each tile's work
+// barely changes); among them the nearest M on a log scale, the larger on a tie.  The split-K reduction is left to the model,
 // whose price for it grows with the rows summed (at M = 1-4 the in-kernel sum wins over
 // the separate kernel that a plan measured at M = 16 may have used).
 bool neighbour_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce) {

@@ -64,7 +64,7 @@ bool tuned_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *redu
 // For M <= kNeighbourMaxM without a plan of its own: the plan measured for the nearest
 // tuned M (same dtype, B layout, N and K, same number of tile rows), if any, with
 // *reduce = -1 (the model picks the reduction).
-constexpr int64_t kNeighbourMaxM = 256;
+constexpr int64_t kNeighbourMaxM = 2048;
 bool neighbour_plan(const Problem &p, int32_t *config, int32_t *split, int32_t *reduce);
 
 // Best plan: a tuned plan for this exact shape if one applies, else a neighbour's

@@ -20,11 +20,15 @@ the choice is made on those times.
 
 Shapes default to the paper-shaped workload sweep (see inputs.py) with B
 row-major, plus the skinny and 8192^3 workloads with B stored column-major
-(the *_bt entry points).  A shapes file lists [dtype, M, K, N] or
-[dtype, M, K, N, "bt"].  Memory-bound shapes (M < 256) are timed cold: the
-launches rotate through enough copies of B to exceed the 256 MB last-level
-cache.  The two cache-sized workloads (int8 256^3, bf16 1024^3) are timed as
-lone launches after a 512 MiB flush.  Back-to-back launches queue behind a
+(the *_bt entry points), and the decode and prefill rows of transformer
+projection sizes with both layouts.  A shapes file lists [dtype, M, K, N] or
+[dtype, M, K, N, "bt"].  Memory-bound shapes (M < 256) are timed with B cold:
+the launches rotate through enough copies of B to exceed the 256 MB last-level
+cache.  So are the decode and prefill rows of the default list at every size
+(a layer's weights come from HBM), and with --cold every shape; the square and
+rectangle workloads are timed warm, as the benchmark times them.  The two
+cache-sized workloads (int8 256^3, bf16 1024^3) are timed as lone launches
+after a 512 MiB flush.  Back-to-back launches queue behind a
 spin kernel so that short kernels are timed on the GPU, not on the host's
 launch rate.
 """
@@ -113,13 +117,16 @@ def _time_sustained(fn, copies, warmup, iters):
 
 
 def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bool = False,
-               confirm: int = 3, rounds: int = 3, cold_single: bool = False):
+               confirm: int = 3, rounds: int = 3, cold_single: bool = False, cold_b: bool = False):
+    """cold_b: B comes from HBM at every launch (launches rotate through copies of B past
+    the last-level cache), as a layer's weights do in a model's forward pass; always the
+    case below 256 rows, where reading B is most of the work."""
     import torch
     from . import binding as b
     d = b.GEMM_DTYPE_I8_I32 if dtype == "int8" else b.GEMM_DTYPE_BF16_F32
     e = 1 if dtype == "int8" else 2
     dev = torch.device("cuda:0")
-    copies = 1 if M >= 256 else int(np.ceil(600e6 / (K * N * e)))
+    copies = int(np.ceil(600e6 / (K * N * e))) if (M < 256 or cold_b) else 1
     b_shape, ldb = ((N, K), K) if bt else ((K, N), N)
     if dtype == "int8":
         A = torch.randint(-128, 128, (M, K), dtype=torch.int8, device=dev)
@@ -192,7 +199,8 @@ def tune_shape(dtype: str, M: int, N: int, K: int, iters: int, log=print, bt: bo
         b.gemm_force_plan(d, b.GEMM_KERNEL_AUTO, -1, 0)
         b.gemm_force_reduce(d, -1)
     best = min(top, key=lambda r: r.get("us_sustained", r["us"]))
-    log(f"{dtype} M={M} K={K} N={N}{' (B column-major)' if bt else ''}: best {best['name']} split {best['split']} reduce {best['reduce']} "
+    log(f"{dtype} M={M} K={K} N={N}{' (B column-major)' if bt else ''}{' (B cold)' if copies > 1 else ''}: "
+        f"best {best['name']} split {best['split']} reduce {best['reduce']} "
         f"{best.get('us_sustained', best['us']):.1f} us sustained, {best['us']:.1f} us burst ({len(results)} plans)")
     del A, Bs, C
     torch.cuda.empty_cache()
@@ -232,6 +240,9 @@ def main():
     ap.add_argument("--plans-out", default=None, help="write the plans as a run-time plan file (gemm_load_plans)")
     ap.add_argument("--json", default=None, help="also write every measurement here")
     ap.add_argument("--iters", type=int, default=15, help="launches per plan in the screening burst")
+    ap.add_argument("--cold", action="store_true",
+                    help="time every shape with B cold (default: below 256 rows, and in the default shape "
+                         "list every shape but the benchmark's warm-timed workloads)")
     ap.add_argument("--confirm", type=int, default=3,
                     help="re-time this many of the fastest plans in the sustained regime and choose among them")
     args = ap.parse_args()
@@ -242,15 +253,21 @@ def main():
         shapes = [tuple(s) for s in inputs.ALL_CONFIGS + extra]
         shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + extra + [c for c in inputs.SQUARE if c[1] == 8192]]
         shapes = list(dict.fromkeys(shapes))        # the rectangle workloads recur among the prefill rows
+        # The benchmark times its square and rectangle workloads warm (B resident in the
+        # last-level cache); every other shape models a layer whose weights come from HBM.
+        warm = set(map(tuple, inputs.SQUARE + inputs.RECT))
     else:
         shapes = [tuple(s) for s in json.load(open(args.shapes))]
+        warm = None
     entries, everything = [], []
     for shape in shapes:
         dtype, M, K, N = shape[:4]
         bt = len(shape) > 4 and shape[4] == "bt"
         # Shapes whose operands fit in the caches are timed as lone launches on cold caches.
         cold_single = (dtype, M, K, N) in inputs.SMALL
-        best, res = tune_shape(dtype, M, N, K, args.iters, bt=bt, confirm=args.confirm, cold_single=cold_single)
+        cold_b = args.cold or (warm is not None and (dtype, M, K, N) not in warm)
+        best, res = tune_shape(dtype, M, N, K, args.iters, bt=bt, confirm=args.confirm, cold_single=cold_single,
+                               cold_b=cold_b)
         entries.append({"dtype": 0 if dtype == "int8" else 1, "M": M, "N": N, "K": K, "trans_b": int(bt), **best})
         everything.append({"dtype": dtype, "M": M, "K": K, "N": N, "bt": bt, "results": res})
     out = args.out or (None if args.plans_out else OUT)

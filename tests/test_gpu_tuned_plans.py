@@ -1,9 +1,9 @@
 """Every measured plan of the decode and prefill shapes (M <= 2048), run at its own shape,
-and the plans that other row counts up to 256 borrow from them (needs an MI355X).
+and the plans that other row counts up to 2048 borrow from them (needs an MI355X).
 
 The tuned plan table maps exact shapes to (configuration, split, reduction); these are
-the plans a caller of those shapes gets, and a shape with M <= 256 and no plan of its own
-at the same N and K borrows the one of the nearest tuned M.  Each is run through the C ABI
+the plans a caller of those shapes gets, and a shape with M <= 2048 and no plan of its own
+at the same N and K borrows the one of the nearest tuned M with as many tile rows.  Each is run through the C ABI
 with the selector's own choice (no override), on seeded inputs, and compared with the
 oracle: int8 element by element, bf16 by the normalised error; the whole C up to 64 rows,
 sampled rows above (int8 also by Freivalds' test over the whole C).  Larger shapes of the
@@ -42,7 +42,7 @@ TABLE_ENTRIES = sorted((e for e in _entries() if e[1] <= 2048), key=_order)
 # (dtype, M, N, K, B layout) at each (dtype, layout, N, K) with skinny tuned plans, for row
 # counts without a plan of their own
 _GROUPS = {(e[0], e[2], e[3], e[7]) for e in TABLE_ENTRIES if e[1] <= 64}
-BORROWED = sorted({(d, M, N, K, bt) for (d, N, K, bt) in _GROUPS for M in (3, 12, 40, 96, 192)} -
+BORROWED = sorted({(d, M, N, K, bt) for (d, N, K, bt) in _GROUPS for M in (3, 12, 40, 96, 192, 480, 2000)} -
                   {(e[0], e[1], e[2], e[3], e[7]) for e in TABLE_ENTRIES}, key=_order)
 FULL_ROWS = 64
 

@@ -152,19 +152,19 @@ def test_tuned_plans_are_valid_and_used():
         check_invariants(p, d, M, N, K)
 
 
-def test_short_shapes_borrow_the_nearest_tuned_plan():
-    """M <= 256 without a plan of its own, at a (dtype, B layout, N, K) that has tuned plans:
+def test_shapes_borrow_the_nearest_tuned_plan():
+    """M <= 2048 without a plan of its own, at a (dtype, B layout, N, K) that has tuned plans:
     the configuration and split of the tuned plan with the nearest M on a log scale (the
     larger M on a tie) among those whose tile covers as many tile rows at both sizes."""
     groups = {}
     for (d, M, N, K, cfg, split, reduce, bt) in _tuned_entries():
-        if M <= 256:
+        if M <= 2048:
             groups.setdefault((d, bt, N, K), {})[M] = (cfg, split)
     checked = 0
     for (d, bt, N, K), by_m in groups.items():
         pl = plan_bt if bt else plan
         bm = {m: pl(d, m, N, K)["bm"] for m in by_m}
-        for M in range(1, 257):
+        for M in list(range(1, 257)) + list(range(260, 2049, 4)):
             if M in by_m:
                 continue
             p = pl(d, M, N, K)
@@ -175,7 +175,7 @@ def test_short_shapes_borrow_the_nearest_tuned_plan():
             near = min(same_rows, key=lambda m: (abs(math.log(m / M)), -m))
             assert (p["config"], p["split_k"]) == by_m[near], (d, bt, M, N, K, p["name"], near)
             checked += 1
-    assert checked >= 4000
+    assert checked >= 10000
 
 
 def test_tuned_plans_skip_misaligned_operands():
