@@ -256,7 +256,7 @@ int gemm_force_plan(int dtype, int kernel, int config, int split_k);
  * blanks -- dtype M N K config split_k reduce trans_b -- the fields of the
  * compiled plan table (reduce: a GEMM_REDUCE_* value, or -1 for the selector's
  * choice; trans_b: 1 for the *_bt calls); '#' starts a comment that runs to the
- * end of the line.  `python -m paper_2512_13282_amd.tune --plans-out FILE`
+ * end of the line; a line holds at most 510 characters.  `python -m paper_2512_13282_amd.tune --plans-out FILE`
  * writes this format.  For exactly those shapes and B layouts the loaded plans
  * take precedence over the compiled table and the model, in this process; a
  * call whose operands the plan's configuration cannot run (alignment) uses the

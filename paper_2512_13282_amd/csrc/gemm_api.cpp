@@ -86,8 +86,9 @@ bool parse_field(char **s, long long lo, long long hi, long long *v) {
 
 // Reads a plan file: one plan per line, "dtype M N K config split reduce trans_b" (the
 // fields of the compiled table), '#' to the end of a line is a comment, blank lines
-// are skipped.  All or nothing: any unreadable file, malformed or out-of-range line
-// leaves `out` unused and returns GEMM_ERR_INVALID_VALUE.
+// are skipped, lines are at most 510 characters.  An unreadable file or a malformed,
+// out-of-range or overlong line returns GEMM_ERR_INVALID_VALUE, and the caller then
+// loads none of the file.
 int read_plan_file(const char *path, std::vector<std::pair<Shape, LoadedPlan>> *out) {
     if (path == nullptr) return GEMM_ERR_INVALID_VALUE;
     FILE *f = fopen(path, "r");
