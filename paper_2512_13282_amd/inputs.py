@@ -85,3 +85,7 @@ MORE_LAYER_KN = ((4096, 6144), (4096, 4096), (8192, 28672), (28672, 8192), (8192
 MORE_LAYERS = [(d, M, K, N) for (K, N) in MORE_LAYER_KN for d in DTYPES for M in (1, 16, 64, 128, 256)]
 # Longer prefill chunks (512 and 2048 rows) at all eleven sizes.
 PREFILL_LONG = [(d, M, K, N) for (K, N) in LAYER_KN + MORE_LAYER_KN for d in DTYPES for M in (512, 2048)]
+# Sizes that are not powers of two (hidden size 3584: feed-forward 18944 and its
+# transpose, fused query/key/value 4608), at every row count above.
+ODD_LAYER_KN = ((3584, 18944), (18944, 3584), (3584, 4608))
+ODD_LAYERS = [(d, M, K, N) for (K, N) in ODD_LAYER_KN for d in DTYPES for M in (1, 16, 64, 128, 256, 512, 2048)]

@@ -249,7 +249,7 @@ def main():
     sys.path.insert(0, os.path.dirname(PKG))
     from . import inputs
     if args.shapes == "default":
-        extra = inputs.DECODE + inputs.PREFILL + inputs.MORE_LAYERS + inputs.PREFILL_LONG
+        extra = inputs.DECODE + inputs.PREFILL + inputs.MORE_LAYERS + inputs.PREFILL_LONG + inputs.ODD_LAYERS
         shapes = [tuple(s) for s in inputs.ALL_CONFIGS + extra]
         shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + extra + [c for c in inputs.SQUARE if c[1] == 8192]]
         shapes = list(dict.fromkeys(shapes))        # the rectangle workloads recur among the prefill rows
