@@ -30,6 +30,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 constexpr int kProbeWaves = 8;
 constexpr int kProbeLds = 96 * 1024;      // more than half the CU's LDS: one workgroup per CU
 
+// 32-bit integer hash: Chris Wellons' "lowbias32" xor-shift-multiply mixer (constants
+// from his hash-prospector search), used only to draw probe operands.
 __device__ __forceinline__ unsigned mix32(unsigned x) {
     x ^= x >> 16;
     x *= 0x7feb352du;
