@@ -43,6 +43,7 @@ struct Key {
         return dtype == o.dtype && M == o.M && N == o.N && K == o.K && vec == o.vec && trans_b == o.trans_b;
     }
 };
+// 64-bit FNV-1a over the key's fields (its published offset basis and prime).
 struct KeyHash {
     size_t operator()(const Key &k) const {
         uint64_t h = 1469598103934665603ULL;
