@@ -86,6 +86,7 @@ MORE_LAYERS = [(d, M, K, N) for (K, N) in MORE_LAYER_KN for d in DTYPES for M in
 # Longer prefill chunks (512 and 2048 rows) at all eleven sizes.
 PREFILL_LONG = [(d, M, K, N) for (K, N) in LAYER_KN + MORE_LAYER_KN for d in DTYPES for M in (512, 2048)]
 # Sizes that are not powers of two (hidden size 3584: feed-forward 18944 and its
-# transpose, fused query/key/value 4608), at every row count above.
-ODD_LAYER_KN = ((3584, 18944), (18944, 3584), (3584, 4608))
+# transpose, fused query/key/value 4608; hidden size 5120: 13824, its transpose and
+# 15360), at every row count above.
+ODD_LAYER_KN = ((3584, 18944), (18944, 3584), (3584, 4608), (5120, 13824), (13824, 5120), (5120, 15360))
 ODD_LAYERS = [(d, M, K, N) for (K, N) in ODD_LAYER_KN for d in DTYPES for M in (1, 16, 64, 128, 256, 512, 2048)]
