@@ -232,6 +232,18 @@ def write_plan_file(entries, path):
         f.write("\n".join(lines) + "\n")
 
 
+def default_shapes():
+    """The default shape list, as (dtype, M, K, N[, "bt"]) tuples, and the set of
+    (dtype, M, K, N) timed with B warm: the benchmark's square and rectangle workloads,
+    which it times warm; every other shape models a layer whose weights come from HBM."""
+    from . import inputs
+    extra = inputs.DECODE + inputs.PREFILL + inputs.MORE_LAYERS + inputs.PREFILL_LONG + inputs.ODD_LAYERS
+    shapes = [tuple(s) for s in inputs.ALL_CONFIGS + extra]
+    shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + extra + [c for c in inputs.SQUARE if c[1] == 8192]]
+    shapes = list(dict.fromkeys(shapes))        # the rectangle workloads recur among the prefill rows
+    return shapes, set(map(tuple, inputs.SQUARE + inputs.RECT))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--shapes", default="default", help="'default' or a JSON file of [dtype, M, K, N] lists")
@@ -249,13 +261,7 @@ def main():
     sys.path.insert(0, os.path.dirname(PKG))
     from . import inputs
     if args.shapes == "default":
-        extra = inputs.DECODE + inputs.PREFILL + inputs.MORE_LAYERS + inputs.PREFILL_LONG + inputs.ODD_LAYERS
-        shapes = [tuple(s) for s in inputs.ALL_CONFIGS + extra]
-        shapes += [tuple(s) + ("bt",) for s in inputs.SKINNY + extra + [c for c in inputs.SQUARE if c[1] == 8192]]
-        shapes = list(dict.fromkeys(shapes))        # the rectangle workloads recur among the prefill rows
-        # The benchmark times its square and rectangle workloads warm (B resident in the
-        # last-level cache); every other shape models a layer whose weights come from HBM.
-        warm = set(map(tuple, inputs.SQUARE + inputs.RECT))
+        shapes, warm = default_shapes()
     else:
         shapes = [tuple(s) for s in json.load(open(args.shapes))]
         warm = None

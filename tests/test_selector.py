@@ -178,6 +178,18 @@ def test_shapes_borrow_the_nearest_tuned_plan():
     assert checked >= 10000
 
 
+def test_tuned_table_is_the_tuner_default_list():
+    """The compiled table holds one measured plan for every shape of the tuner's default
+    list and nothing else, so re-running the tuner with no arguments reproduces it."""
+    from paper_2512_13282_amd import tune
+    shapes, warm = tune.default_shapes()
+    want = {(DT[s[0]], s[1], s[3], s[2], int(len(s) > 4)) for s in shapes}
+    have = [(d, M, N, K, bt) for (d, M, N, K, cfg, split, reduce, bt) in _tuned_entries()]
+    assert len(have) == len(set(have)), "a shape appears twice"
+    assert set(have) == want
+    assert all((s[0], s[1], s[2], s[3]) in inputs.ALL_CONFIGS for s in warm)
+
+
 def test_tuned_plans_skip_misaligned_operands():
     # the same shape with a misaligned A pointer falls back to the alignment-agnostic family
     (d, M, N, K, cfg, split, reduce, bt) = _tuned_entries()[0]
