@@ -114,8 +114,19 @@ typedef struct gemm_plan_info {
                                     (A ~ MNK/BN, B ~ MNK/BM), C, partials      */
     double  model_t_comp_us; /* modelled MFMA time at the plan's efficiency    */
     double  model_t_mem_us;  /* modelled memory time (sustained HBM rate, L2 re-reads) */
+    int32_t source;          /* where the plan came from: GEMM_PLAN_FROM_*      */
     char    name[48];        /* human-readable kernel/config name              */
 } gemm_plan_info;
+
+/* Where a plan came from (gemm_plan_info.source). */
+enum {
+    GEMM_PLAN_FROM_MODEL = 0,     /* the balance model (no measured plan applies)           */
+    GEMM_PLAN_FROM_TABLE = 1,     /* the compiled table of measured plans, this exact shape */
+    GEMM_PLAN_FROM_NEIGHBOUR = 2, /* the table's plan for the nearest M at this N, K (same
+                                     number of tile rows; M <= 2048)                        */
+    GEMM_PLAN_FROM_FILE = 3,      /* a plan loaded by gemm_load_plans / GEMM_MI355X_PLANS   */
+    GEMM_PLAN_FROM_FORCED = 4     /* gemm_force_plan / gemm_force_reduce                    */
+};
 
 /* Split-K reductions (gemm_plan_info.reduce_in_kernel, gemm_force_reduce). */
 enum {

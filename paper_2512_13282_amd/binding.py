@@ -45,6 +45,8 @@ GEMM_REDUCE_SEPARATE = 0
 GEMM_REDUCE_LAST_SLICE = 1
 GEMM_REDUCE_ATOMIC = 2
 GEMM_REDUCE_ATOMIC_FLAG = 3
+# gemm_plan_info.source
+GEMM_PLAN_FROM_MODEL, GEMM_PLAN_FROM_TABLE, GEMM_PLAN_FROM_NEIGHBOUR, GEMM_PLAN_FROM_FILE, GEMM_PLAN_FROM_FORCED = range(5)
 
 EXPORTED = ("gemm_i8_i32", "gemm_bf16_f32", "gemm_i8_i32_bt", "gemm_bf16_f32_bt",
             "gemm_i8_i8", "gemm_i8_i16", "gemm_bf16_bf16", "gemm_i8_i8_bt", "gemm_i8_i16_bt",
@@ -65,6 +67,7 @@ class PlanInfo(ctypes.Structure):
         ("lds_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
         ("model_traffic_bytes", ctypes.c_double),
         ("model_t_comp_us", ctypes.c_double), ("model_t_mem_us", ctypes.c_double),
+        ("source", ctypes.c_int32),
         ("name", ctypes.c_char * 48),
     ]
 

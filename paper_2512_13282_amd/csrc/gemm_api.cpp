@@ -53,7 +53,11 @@ struct KeyHash {
         return size_t(h);
     }
 };
-std::unordered_map<Key, Plan, KeyHash> g_cache;
+struct CachedPlan {
+    Plan plan;
+    int32_t source;   // GEMM_PLAN_FROM_*
+};
+std::unordered_map<Key, CachedPlan, KeyHash> g_cache;
 
 // Plans loaded at run time (gemm_load_plans, GEMM_MI355X_PLANS), per exact shape and
 // B layout; they take precedence over the compiled table.  Guarded by g_mu.
@@ -177,7 +181,8 @@ int validate(const Problem &p, const void *A, const void *B, const void *C, int6
     return GEMM_OK;
 }
 
-int plan_for(const Problem &p, Plan *out) {
+// The plan for a call, and where it came from (GEMM_PLAN_FROM_*) if `source` is given.
+int plan_for(const Problem &p, Plan *out, int32_t *source = nullptr) {
     std::call_once(g_env_once, load_env_plans);
     Override ov;
     {
@@ -190,7 +195,8 @@ int plan_for(const Problem &p, Plan *out) {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_cache.find(key);
         if (it != g_cache.end()) {
-            *out = it->second;
+            *out = it->second.plan;
+            if (source) *source = it->second.source;
             return GEMM_OK;
         }
     }
@@ -210,13 +216,21 @@ int plan_for(const Problem &p, Plan *out) {
     }
     if (!loaded && !gemm::select_plan(p, &pl, ov.family, ov.config, ov.split, gemm::Chip(), ov.reduce))
         return GEMM_ERR_UNSUPPORTED;
+    // select_plan consults the compiled table, then the nearest-M neighbours, then the model.
+    int32_t cfg, split, reduce;
+    const int32_t src = forced ? GEMM_PLAN_FROM_FORCED
+                      : loaded ? GEMM_PLAN_FROM_FILE
+                      : gemm::tuned_plan(p, &cfg, &split, &reduce) ? GEMM_PLAN_FROM_TABLE
+                      : gemm::neighbour_plan(p, &cfg, &split, &reduce) ? GEMM_PLAN_FROM_NEIGHBOUR
+                      : GEMM_PLAN_FROM_MODEL;
     if (!forced) {
         const Key key{p.dtype, p.M, p.N, p.K, gemm::vector_loads_ok(p), p.trans_b};
         std::lock_guard<std::mutex> lk(g_mu);
         if (g_cache.size() > 4096) g_cache.clear();
-        g_cache.emplace(key, pl);
+        g_cache.emplace(key, CachedPlan{pl, src});
     }
     *out = pl;
+    if (source) *source = src;
     return GEMM_OK;
 }
 
@@ -340,7 +354,8 @@ static int plan_impl(int dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K
         return GEMM_OK;
     }
     Plan pl;
-    rc = plan_for(p, &pl);
+    int32_t source = GEMM_PLAN_FROM_MODEL;
+    rc = plan_for(p, &pl, &source);
     if (rc != GEMM_OK) return rc;
     const gemm::TileConfig &c = gemm::kConfigs[pl.config];
     out->kernel = c.family;
@@ -362,6 +377,7 @@ static int plan_impl(int dtype, int32_t trans_b, int64_t M, int64_t N, int64_t K
     out->model_traffic_bytes = pl.traffic_bytes;
     out->model_t_comp_us = pl.t_comp_us;
     out->model_t_mem_us = pl.t_mem_us;
+    out->source = source;
     strncpy(out->name, c.name, sizeof(out->name) - 1);
     return GEMM_OK;
 }

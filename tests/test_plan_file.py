@@ -172,3 +172,19 @@ def test_the_tuner_writes_files_that_load(tmp_path):
     assert b.gemm_load_plans(path) == b.GEMM_OK
     assert triple(plan(I8, 100, 1024, 3072)) == (30, 3, b.GEMM_REDUCE_SEPARATE)
     assert triple(plan(BF, 48, 2048, 5120, bt=True))[:2] == (20, 4)
+
+
+def test_plan_source_is_reported(tmp_path):
+    """gemm_plan_info.source says where each plan came from."""
+    assert plan(I8, 1, 14336, 4096)["source"] == b.GEMM_PLAN_FROM_TABLE          # a shape of the table
+    assert plan(I8, 3, 14336, 4096)["source"] == b.GEMM_PLAN_FROM_NEIGHBOUR      # borrows M = 1's or 8's
+    assert plan(I8, 3, 14336 + 128, 4096)["source"] == b.GEMM_PLAN_FROM_MODEL    # no plans at this N
+    assert plan(I8, 1, 14336, 4096, off=1)["source"] == b.GEMM_PLAN_FROM_MODEL   # misaligned: generic kernel
+    assert b.gemm_load_plans(write(tmp_path, "0 100 1024 3072 30 3 0 0\n")) == b.GEMM_OK
+    assert plan(I8, 100, 1024, 3072)["source"] == b.GEMM_PLAN_FROM_FILE
+    try:
+        assert b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, 31, 2) == b.GEMM_OK
+        assert plan(I8, 100, 1024, 3072)["source"] == b.GEMM_PLAN_FROM_FORCED
+    finally:
+        b.gemm_force_plan(I8, b.GEMM_KERNEL_AUTO, -1, 0)
+    assert plan(I8, 100, 1024, 3072)["source"] == b.GEMM_PLAN_FROM_FILE          # cached with its source
