@@ -47,6 +47,7 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"int8": 5000.0, "bf16": 2500.0}          # dense MFMA, TOPS / TFLOP/s (AMD published)
 REDUCE_NAMES = {0: "separate", 1: "last-slice", 2: "atomic", 3: "atomic-flag"}   # split-K reductions (GEMM_REDUCE_*)
+PLAN_SOURCES = {0: "model", 1: "measured (table)", 2: "measured (nearest M)", 3: "measured (plan file)", 4: "forced"}   # gemm_plan_info.source (GEMM_PLAN_FROM_*)
 CONFIG_ORACLE_SECONDS = 0.25  # CPU oracle work per row of the workload table (`cpu_oracle`)
 HBM_GBS = 8000.0
 KERNEL_DIR = os.path.join(ROOT, "paper_2512_13282_amd", "csrc")
@@ -311,6 +312,7 @@ def summarize(w: Workload, ms_step: float, k_avg: float, k_min: float):
         "pct_dense_peak": round(100.0 * value / PEAK[w.dtype], 2),
         "plan": plan["name"], "split_k": plan["split_k"], "grid": plan["grid"],
         "reduce": REDUCE_NAMES[plan["reduce_in_kernel"]] if plan["split_k"] > 1 else None,
+        "plan_source": PLAN_SOURCES.get(plan.get("source"), "?"),
         "algorithmic_ops_per_launch": ops, "algorithmic_bytes_per_launch": comp_bytes,
         "roofline": roof,
     }
@@ -423,7 +425,8 @@ def config_table(skip, steps: int, warmup: int, oracle_seconds: float = 0.0, set
         ops = 2.0 * M * N * K
         bare = bare_read_us(w) if skinny else None
         row = {"dtype": dtype, "M": M, "K": K, "N": N, "protocol": proto, "plan": r["plan"],
-               "split_k": r["split_k"], "reduce": r["reduce"], "kernel_us": round(kavg * 1e3, 2),
+               "split_k": r["split_k"], "reduce": r["reduce"], "plan_source": r["plan_source"],
+               "kernel_us": round(kavg * 1e3, 2),
                "value": round(ops / (kavg * 1e-3) / 1e12, 2), "unit": r["unit"],
                "pct_dense_peak": round(100.0 * ops / (kavg * 1e-3) / 1e12 / PEAK[dtype], 2),
                "roofline": {k: r["roofline"][k] for k in ("bound", "achieved", "unit", "frac")},
