@@ -101,6 +101,9 @@ def parse():
     ap.add_argument("--workload", default=None, metavar="DTYPE:MxKxN",
                     help="time only this workload (e.g. int8:2048x2048x2048) with --steps/--warmup and print "
                          "one JSON line (for profiling one kernel)")
+    ap.add_argument("--cold", action="store_true",
+                    help="with --workload: rotate the launches through copies of B so that more than 512 MB "
+                         "is read between reuses of one (B from HBM, as a layer's weights arrive)")
     return ap.parse_args()
 
 
@@ -681,10 +684,13 @@ def main():
     if args.workload:
         dtype, shape = args.workload.split(":")
         M, K, N = (int(x) for x in shape.split("x"))
-        w = Workload(dtype, M, N, K)
+        e = 1 if dtype == "int8" else 2
+        copies = max(1, int(np.ceil(512e6 / (K * N * e))) + 1) if args.cold else 1
+        w = Workload(dtype, M, N, K, copies=copies)
         ms, kavg, kmin = time_workload(w, args.steps, args.warmup, args.settle_ms)
         r = summarize(w, ms, kavg, kmin)
-        r.update({"workload": args.workload, "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))})
+        r.update({"workload": args.workload, "b_copies": copies,
+                  "parity_sample_ok": parity_sample(w, sorted({0, M // 2, M - 1}))})
         print(json.dumps(r), flush=True)
         return
 
